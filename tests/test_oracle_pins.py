@@ -1,0 +1,363 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Nothing here compares the oracle with itself: every expected value comes from a
+closed form, a hand-worked example, an independent library route (PyTorch's
+CPU bf16 cast, float64 arithmetic, Python's decimal module) or brute force.
+
+Reading of the reduction (Sec. 3.1 "Oneshot"; the pull-and-reduce listing of
+Sec. 4.2): peers are added in ascending rank order into one result. Payloads
+are bf16, the accumulator fp32 (IEEE add, round-to-nearest-even, subnormals
+kept) and the fp32 sum is rounded once more, to bf16, ties to even.
+"""
+from __future__ import annotations
+
+import decimal
+import os
+import struct
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import ref_np
+
+
+def f32(u: int) -> float:
+    return struct.unpack("<f", struct.pack("<I", u))[0]
+
+
+def torch_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Library route: fp32 -> bf16 with PyTorch's CPU cast (RNE)."""
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def torch_bf16_value(b: np.ndarray) -> np.ndarray:
+    t = torch.from_numpy(np.ascontiguousarray(b, dtype=np.uint16).view(np.int16))
+    return t.view(torch.bfloat16).to(torch.float64).numpy()
+
+
+ALL16 = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+NONNAN16 = ALL16[~np.isnan(torch_bf16_value(ALL16))]
+
+
+# --------------------------------------------------------------------------
+# Floating-point environment and the two conversions
+
+
+def test_fp_environment():
+    assert oracle.fp_env_ok(), "oracle needs round-to-nearest with no FTZ/DAZ"
+
+
+def test_decode_every_bf16_pattern_matches_library():
+    got = oracle.bf16_value_array(ALL16)
+    exp = torch_bf16_value(ALL16)
+    nan = np.isnan(exp)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], exp[~nan])
+    # signed zeros decode with their sign
+    assert np.signbit(got[0x8000]) and not np.signbit(got[0x0000])
+
+
+def _stratified_f32_patterns() -> np.ndarray:
+    """Every high half with low halves at and around the rounding boundary."""
+    hi = np.arange(65536, dtype=np.uint32) << 16
+    lows = np.array([0x0000, 0x0001, 0x3FFF, 0x7FFE, 0x7FFF, 0x8000, 0x8001, 0xBFFF,
+                     0xFFFE, 0xFFFF], dtype=np.uint32)
+    rnd = np.random.default_rng(5).integers(0, 65536, 6, dtype=np.uint32)
+    return (hi[:, None] | np.concatenate([lows, rnd])[None, :]).ravel()
+
+
+def test_round_f32_stratified_matches_library():
+    u = _stratified_f32_patterns()
+    x = u.view(np.float32)
+    exp = torch_bf16_bits(x)
+    with np.errstate(invalid="ignore"):
+        got_c = oracle.bf16_round_array(x.astype(np.float64))
+    got_np = ref_np.narrow_rne_f32(x)
+    nan = np.isnan(x)
+    for got in (got_c, got_np):
+        assert np.array_equal(got[~nan], exp[~nan])
+        v = torch_bf16_value(got[nan])
+        assert np.all(np.isnan(v)), "a NaN in gives a NaN out"
+
+
+@pytest.mark.parametrize("u, exp", [
+    (0x3F808000, 0x3F80),  # 1 + 2^-8: exact tie, kept LSB even -> down
+    (0x3F818000, 0x3F82),  # 1 + 3*2^-8: tie, odd LSB -> up
+    (0x3F808001, 0x3F81),  # just above the tie -> up
+    (0x3F807FFF, 0x3F80),  # just below the tie -> down
+    (0x7F7FFFFF, 0x7F80),  # largest float rounds past the largest bf16 -> inf
+    (0x7F7F7FFF, 0x7F7F),  # stays at the largest finite bf16
+    (0x00000001, 0x0000),  # 2^-149 is far below half the smallest bf16 subnormal
+    (0x00008000, 0x0000),  # 2^-134: tie between 0 and 2^-133 -> even (0)
+    (0x00018000, 0x0002),  # 1.5 * 2^-133: tie, odd -> up to 2 * 2^-133
+    (0x00010000, 0x0001),  # smallest bf16 subnormal is kept (no flush)
+    (0x807FFFFF, 0x8080),  # largest negative subnormal rounds up to -2^-126
+    (0x80000000, 0x8000),  # -0 keeps its sign
+])
+def test_round_hand_cases(u, exp):
+    assert oracle.bf16_round(f32(u)) == exp
+    assert int(ref_np.narrow_rne_f32(np.array([f32(u)], np.float32))[0]) == exp
+
+
+def test_round_from_double_single_rounding():
+    # 1 + 2^-8 + 2^-30 is above the tie: one rounding gives 0x3F81. (Going
+    # through float32 first would land on the tie and give 0x3F80.)
+    assert oracle.bf16_round(1.0 + 2.0 ** -8 + 2.0 ** -30) == 0x3F81
+    assert int(ref_np.narrow_rne_f64(np.array([1.0 + 2.0 ** -8 + 2.0 ** -30]))[0]) == 0x3F81
+
+
+def test_round_f64_brute_force_nearest():
+    """Nearest bf16 by exhaustive search over every finite positive bf16 value."""
+    pos = ALL16[:0x7F80]                       # +0 .. largest finite
+    vals = torch_bf16_value(pos)
+    g = np.random.default_rng(9)
+    xs = np.concatenate([
+        g.standard_normal(2000) * 10.0 ** g.integers(-40, 38, 2000),
+        (vals[1:] + vals[:-1])[::97] / 2.0,    # exact midpoints
+        g.random(200) * 1e-39,                 # subnormal range
+    ])
+    got = oracle.bf16_round_array(xs)
+    got_np = ref_np.narrow_rne_f64(xs)
+    for x, b, bn in zip(xs, got, got_np):
+        a = abs(x)
+        i = int(np.searchsorted(vals, a))
+        cands = [j for j in (i - 1, i) if 0 <= j < len(vals)]
+        best = min(cands, key=lambda j: (abs(vals[j] - a), int(pos[j]) & 1))
+        if a >= vals[-1] + (vals[-1] - vals[-2]) / 2:
+            best_bits = 0x7F80
+        else:
+            best_bits = int(pos[best])
+        if x < 0:
+            best_bits |= 0x8000
+        assert int(b) == best_bits, (x, hex(b), hex(best_bits))
+        assert int(bn) == best_bits
+
+
+# --------------------------------------------------------------------------
+# The reduction
+
+
+@pytest.mark.parametrize("n, exp", [(1, 0x3F80), (2, 0x4000), (3, 0x4040), (4, 0x4080),
+                                    (5, 0x40A0), (6, 0x40C0), (7, 0x40E0), (8, 0x4100)])
+def test_all_ones_sum_to_n(n, exp):
+    x = np.full((n, 4096), 0x3F80, np.uint16)
+    assert np.all(oracle.reduce(x) == exp)
+    assert np.all(ref_np.reduce(x) == exp)
+
+
+def test_single_rank_is_identity():
+    x = NONNAN16[None, :]
+    assert np.array_equal(oracle.reduce(x), x[0])
+
+
+@pytest.mark.parametrize("n", [2, 4, 8])
+def test_single_nonzero_rank_is_identity(n):
+    nz = NONNAN16[(NONNAN16 != 0x0000) & (NONNAN16 != 0x8000)]
+    for r in range(n):
+        x = np.zeros((n, nz.size), np.uint16)
+        x[r] = nz
+        assert np.array_equal(oracle.reduce(x), nz)
+
+
+def test_small_integers_are_exact():
+    g = np.random.default_rng(3)
+    for n in range(1, 9):
+        ints = g.integers(-32, 33, (n, 5000))
+        x = torch_bf16_bits(ints.astype(np.float32))
+        exp = torch_bf16_bits(ints.sum(axis=0).astype(np.float32))
+        assert np.array_equal(oracle.reduce(x), exp)
+
+
+@pytest.mark.parametrize("xs, exp", [
+    # fp32 sum 1 + 2^-8 (2^-30 is lost in fp32) is a bf16 tie -> even 0x3F80;
+    # rounding the exact sum once would give 0x3F81: the reading is a double rounding.
+    ([0x3F80, 0x3B80, 0x3080], 0x3F80),
+    # order matters under cancellation: 100 - 100 + 2^-20 = 2^-20 ...
+    ([0x42C8, 0xC2C8, 0x3580], 0x3580),
+    # ... but 2^-20 - 100 + 100 loses 2^-20 in the first add
+    ([0x3580, 0xC2C8, 0x42C8], 0x0000),
+    ([0x8000, 0x8000], 0x8000),            # -0 + -0 = -0 (accumulator seeded by rank 0)
+    ([0x8000, 0x8000, 0x8000, 0x8000], 0x8000),
+    ([0x8000, 0x0000], 0x0000),            # -0 + +0 = +0
+    ([0x0000, 0x8000], 0x0000),
+    ([0x0001, 0x0001], 0x0002),            # subnormals add exactly, no flush
+    ([0x8001, 0x0001], 0x0000),
+    ([0x7F7F, 0x7F7F], 0x7F80),            # overflow in fp32 -> inf
+    ([0x7F7F, 0x7B00], 0x7F80),            # (2 - 2^-8) * 2^127 exactly: tie -> even = inf
+    ([0x7F7F, 0x7A80], 0x7F7F),            # below the tie: stays finite
+    ([0x7F80, 0xFF80], None),              # inf - inf = NaN
+    ([0x7FC0, 0x3F80], None),              # NaN propagates
+])
+def test_reduce_hand_cases(xs, exp):
+    x = np.array(xs, np.uint16)[:, None]
+    got = int(oracle.reduce(x)[0])
+    got_np = int(ref_np.reduce(x)[0])
+    if exp is None:
+        assert np.isnan(oracle.bf16_value(got)) and np.isnan(oracle.bf16_value(got_np))
+    else:
+        assert got == exp and got_np == exp
+
+
+def _pairs_check(a: np.ndarray, b: np.ndarray, use_c: bool):
+    """N=2 against the float64 route: float32(float64(a) + float64(b)) is the
+    correctly rounded fp32 sum (double rounding is innocuous for one add when
+    the wide format has >= 2p + 2 bits, 53 >= 50), then PyTorch's bf16 cast."""
+    x = np.stack([a, b])
+    with np.errstate(over="ignore", invalid="ignore"):
+        s = (ref_np.widen(a).astype(np.float64) + ref_np.widen(b).astype(np.float64)).astype(np.float32)
+    exp = torch_bf16_bits(s)
+    nan = np.isnan(s)
+    got = oracle.reduce(x) if use_c else ref_np.reduce(x)
+    assert np.array_equal(got[~nan], exp[~nan])
+    assert np.all(np.isnan(torch_bf16_value(got[nan])))
+
+
+def test_pairs_every_a_against_sampled_b():
+    g = np.random.default_rng(17)
+    special = np.array([0x0000, 0x8000, 0x0001, 0x8001, 0x007F, 0x0080, 0x3F80, 0xBF80,
+                        0x7F7F, 0xFF7F, 0x7F80, 0xFF80, 0x3B80, 0xBB80], np.uint16)
+    bs = np.concatenate([special, g.integers(0, 65536, 242, dtype=np.uint32).astype(np.uint16)])
+    for b in bs:
+        _pairs_check(ALL16, np.full(65536, b, np.uint16), use_c=True)
+    a = g.integers(0, 65536, 1 << 22, dtype=np.uint32).astype(np.uint16)
+    b = g.integers(0, 65536, 1 << 22, dtype=np.uint32).astype(np.uint16)
+    _pairs_check(a, b, use_c=False)
+
+
+@pytest.mark.skipif(os.environ.get("SIFAR_EXHAUSTIVE") != "1",
+                    reason="all 2^32 bf16 pairs take ~6 minutes; set SIFAR_EXHAUSTIVE=1")
+def test_pairs_exhaustive():
+    for hi in range(0, 65536, 256):
+        a = np.repeat(np.arange(hi, hi + 256, dtype=np.uint32).astype(np.uint16), 65536)
+        _pairs_check(a, np.tile(ALL16, 256), use_c=False)
+
+
+def test_library_loop_on_workload_data():
+    """PyTorch CPU, explicit fixed-order loop in float32, then the bf16 cast."""
+    import synth
+    for w in (synth.SMOKE_N2, synth.LLAMA8B_DECODE, synth.MOE_DECODE, synth.PAYLOAD_SWEEP[-1]):
+        pool = synth.payload_pool(w.wid, w.nranks, 2, min(w.hidden, 2048), 3, w.dist)
+        for e in range(3):
+            x = pool[e]
+            t = torch.from_numpy(x.view(np.int16)).view(torch.bfloat16)
+            acc = t[0].float()
+            for r in range(1, x.shape[0]):
+                acc = acc + t[r].float()
+            exp = acc.bfloat16().view(torch.int16).numpy().view(np.uint16)
+            assert np.array_equal(oracle.reduce(x), exp)
+            assert np.array_equal(ref_np.reduce(x), exp)
+
+
+# --------------------------------------------------------------------------
+# Residual-add + RMSNorm epilogue (paper silent; fp64 reading)
+
+
+def _ulp_distance(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """Distance in bf16 steps between two bf16 bit arrays (+0 and -0 equal)."""
+    def key(x):
+        x = x.astype(np.int32)
+        return np.where(x & 0x8000, -(x & 0x7FFF), x)
+    return np.abs(key(a) - key(b))
+
+
+def _epilogue_inputs(T, H, seed=0):
+    import synth
+    g = np.random.default_rng(seed)
+    a = synth.bf16(g, (T, H), "act")
+    res = synth.bf16(g, (T, H), "normal")
+    w = synth.bf16(g, (H,), "weight")
+    return a, res, w
+
+
+EPS = float(np.float32(1e-6))
+
+
+def test_epilogue_c_and_numpy_agree_bit_exactly():
+    a, res, w = _epilogue_inputs(5, 1000)
+    r1, y1 = oracle.residual_rmsnorm(a, res, w, EPS)
+    r2, y2 = ref_np.residual_rmsnorm(a, res, w, EPS)
+    assert np.array_equal(r1, r2) and np.array_equal(y1, y2)
+
+
+def test_epilogue_against_torch_composition():
+    a, res, w = _epilogue_inputs(4, 4096, seed=1)
+    r, y = oracle.residual_rmsnorm(a, res, w, EPS)
+    bf = lambda x: torch.from_numpy(x.view(np.int16)).view(torch.bfloat16)
+    r_t = (bf(a).float() + bf(res).float()).bfloat16()
+    assert np.array_equal(r, r_t.view(torch.int16).numpy().view(np.uint16))
+    x = r_t.double()
+    y_t = (x * torch.rsqrt(x.pow(2).mean(-1, keepdim=True) + EPS) * bf(w).double()).float().bfloat16()
+    d = _ulp_distance(y, y_t.view(torch.int16).numpy().view(np.uint16))
+    assert d.max() <= 1
+
+
+def test_epilogue_constant_row_normalises_to_one():
+    # res' = c everywhere, w = 1, eps = 0  ->  y = c / |c| = +-1 exactly.
+    for c in (0x3F80, 0x4040, 0xC1A0, 0x0001, 0x7F00):
+        H = 4096
+        a = np.zeros((1, H), np.uint16)
+        res = np.full((1, H), c, np.uint16)
+        w = np.full(H, 0x3F80, np.uint16)
+        r, y = oracle.residual_rmsnorm(a, res, w, 0.0)
+        assert np.all(r == c)
+        assert np.all(y == (0xBF80 if c & 0x8000 else 0x3F80))
+
+
+def test_epilogue_scale_invariance():
+    # With eps = 0, scaling a row by 2^k scales sum(x^2) by 4^k and the
+    # correctly rounded sqrt by exactly 2^k: y must not change by one bit.
+    a, res, w = _epilogue_inputs(3, 512, seed=2)
+    a[:] = 0                                   # res' = res
+    e = (res >> 7) & 0xFF
+    res = np.where((e > 10) & (e < 240), res, 0).astype(np.uint16)
+    _, y = oracle.residual_rmsnorm(a, res, w, 0.0)
+    for k in (-3, 5):
+        scaled = np.where(res & 0x7FFF, res.astype(np.int32) + (k << 7), res).astype(np.uint16)
+        _, yk = oracle.residual_rmsnorm(a, scaled, w, 0.0)
+        assert np.array_equal(y, yk)
+
+
+def _nearest_bf16_exact(x: decimal.Decimal) -> int:
+    pos = ALL16[:0x7F80]
+    vals = [decimal.Decimal(float(v)) for v in torch_bf16_value(pos)]
+    a = abs(x)
+    lo, hi = 0, len(vals) - 1
+    while lo < hi:                      # first value >= a
+        mid = (lo + hi) // 2
+        if vals[mid] < a:
+            lo = mid + 1
+        else:
+            hi = mid
+    cands = [j for j in (lo - 1, lo) if 0 <= j < len(vals)]
+    best = min(cands, key=lambda j: (abs(vals[j] - a), int(pos[j]) & 1))
+    bits = int(pos[best])
+    return bits | 0x8000 if x < 0 else bits
+
+
+def test_epilogue_tiny_rows_exact_arithmetic():
+    """RMSNorm of tiny rows in 50-digit decimal arithmetic, rounded by search."""
+    decimal.getcontext().prec = 50
+    g = np.random.default_rng(4)
+    for H in (1, 2, 3, 7):
+        a, res, w = _epilogue_inputs(2, H, seed=int(g.integers(1 << 30)))
+        r, y = oracle.residual_rmsnorm(a, res, w, EPS)
+        D = lambda b: decimal.Decimal(float(torch_bf16_value(np.array([b], np.uint16))[0]))
+        for t in range(2):
+            rr = [_nearest_bf16_exact(D(a[t, h]) + D(res[t, h])) for h in range(H)]
+            assert list(r[t]) == rr
+            ss = sum(D(b) * D(b) for b in rr)
+            inv = 1 / (ss / H + decimal.Decimal(EPS)).sqrt()
+            yy = [_nearest_bf16_exact(D(rr[h]) * inv * D(w[h])) for h in range(H)]
+            assert list(y[t]) == yy
+
+
+def test_reduce_chain_uses_pool_entries_cyclically():
+    import synth
+    pool = synth.payload_pool(99, 2, 1, 64, 4, "normal")
+    outs = oracle.reduce_chain(pool, range(1, 10), 1)
+    for g, o in zip(range(1, 10), outs):
+        assert np.array_equal(o, oracle.reduce(pool[(g - 1) % 4][:, :1, :]))
+    assert np.array_equal(outs[0], outs[4])
