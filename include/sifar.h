@@ -1,0 +1,236 @@
+/*
+ * sifar.h -- C ABI of libsifar, a single-GPU (MI355X, gfx950) implementation of
+ * the data path of SiFAR, the synchronization-free one-shot all-reduce
+ * ("SiFAR: Synchronization-Free All-Reduce for Low-Latency LLM Inference").
+ *
+ * What one all-reduce computes (Sec. 3.1 "Oneshot", and the pull-and-reduce
+ * listing of Sec. 4.2): every rank's partial hidden state is pulled and added,
+ * peer after peer in ascending rank order. Here payloads are bf16, the sum is
+ * accumulated in fp32 (IEEE adds, round to nearest even, subnormals kept) and
+ * rounded once to bf16, round to nearest even.
+ *
+ * How it is synchronised:
+ *  - No bottom barrier (Sec. 3.3, 4.1 "Dual Buffering Design"): every rank
+ *    owns two payload slots and two flag ("stamp") slots and alternates
+ *    between them; epoch g uses parity g & 1, so a slot is rewritten only after
+ *    the reduction two epochs back, which stream order has completed.
+ *  - No top barrier (Sec. 3.5, 4.1 "Speculative Reduction Design", 4.2
+ *    "Speculative Reduction"): the reduction loads the payload without
+ *    waiting, validates each rank's stamp against the epoch afterwards, and
+ *    re-runs on a stale stamp. The flag of epoch g is g itself (the paper's
+ *    flag grows by one per all-reduce; Sec. 4.2 "Verification Logic
+ *    Correctness"). The paper compares the SUM of the flags with N * flag;
+ *    this library compares each rank's stamp with g (equivalent under dual
+ *    buffering, and it names the stale ranks).
+ *
+ * The N ranks are emulated on one GPU: each rank's slots are HBM buffers, and
+ * a producer kernel plays the peers, copying each rank's partial into its slot
+ * and then release-storing its stamp. One process, one GPU; nothing crosses a
+ * device boundary.
+ *
+ * Conventions
+ *  - Every function returns int: SIFAR_OK (0) or a negative SIFAR_E* code.
+ *    Nothing aborts, throws or prints.
+ *  - Device pointers are HIP device addresses on the handle's device, 16-byte
+ *    aligned. bf16 values are passed as raw 16-bit patterns. Host pointers are
+ *    ordinary host memory.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *    Enqueueing calls are asynchronous and stream-ordered; only sifar_status()
+ *    and sifar_read_log() synchronise.
+ *  - The library owns the slots, stamps, counters, decision log, injection
+ *    table, error word and captured graphs. The caller owns every buffer it
+ *    passes in and must keep it alive until the enqueued work has finished.
+ *  - One host thread per handle. Calls on one handle must use one stream, or
+ *    streams the caller orders.
+ *  - A device-detected error (retry budget exhausted, slot rewritten before
+ *    it was consumed, epilogue exchange timed out) is latched in device memory
+ *    and reported by the next sifar_status() as SIFAR_EDEVICE; the handle then
+ *    refuses further work (SIFAR_ESTATE) until destroyed.
+ */
+#ifndef SIFAR_H
+#define SIFAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct sifar_ctx *sifar_t;
+
+/* ---- return codes --------------------------------------------------------- */
+#define SIFAR_OK 0
+#define SIFAR_EINVAL (-1)  /* bad argument; nothing was enqueued */
+#define SIFAR_ENOMEM (-2)  /* device or host allocation failed */
+#define SIFAR_EHIP (-3)    /* a HIP runtime call failed */
+#define SIFAR_ESTATE (-4)  /* call out of protocol order, or handle poisoned */
+#define SIFAR_EDEVICE (-5) /* the device latched an error (see sifar_error_info) */
+
+/* device error kinds (sifar_error_info, info[0]) */
+#define SIFAR_DEV_RETRY_BUDGET 1 /* a chunk exhausted max_attempts: its stamps never became fresh */
+#define SIFAR_DEV_WAW 2          /* producer found a slot whose previous epoch was not consumed */
+#define SIFAR_DEV_EXCHANGE 3     /* epilogue: a token's segments did not all arrive within spin_limit */
+
+/* ---- validation modes ------------------------------------------------------
+ * SPEC     the paper's speculative reduction (Sec. 3.5, 4.2): payload and
+ *          stamps are loaded together, validation follows, a stale stamp
+ *          re-runs both. Correct when a rank whose stamp is fresh at
+ *          validation also had its payload in place when it was loaded -- the
+ *          monotonicity assumption of Sec. 8.1.
+ * ORDERED  stamps are acquired first and the payload is loaded only once all
+ *          are fresh: a top barrier by flag polling (the "oneshot + dual
+ *          buffering" configuration of Sec. 3.4). Correct without any
+ *          monotonicity assumption.
+ * NONE     no stamps are read: the idealised "no barrier" configuration of
+ *          Sec. 6.3. Only correct when stream order alone guarantees the data. */
+#define SIFAR_VALIDATE_SPEC 0
+#define SIFAR_VALIDATE_ORDERED 1
+#define SIFAR_VALIDATE_NONE 2
+
+/* ---- stale-stamp injection ---------------------------------------------------
+ * DETERMINISTIC: for epoch g, table entry (g - 1) % entries holds two rank masks:
+ *   bits 0-7  late ranks: the producer writes their payload but not their stamp;
+ *             the stamp lands right after the reduction's first failed
+ *             validation of each chunk (the rank "catches up").
+ *   bits 8-15 withheld ranks: the stamp is never written; the chunk exhausts
+ *             max_attempts and SIFAR_DEV_RETRY_BUDGET is latched.
+ * The resulting per-chunk decisions are exactly predictable (see the log). */
+#define SIFAR_INJECT_OFF 0
+#define SIFAR_INJECT_DETERMINISTIC 1
+
+/* ---- configuration ---------------------------------------------------------- */
+typedef struct {
+    int32_t nranks;           /* N: emulated tensor-parallel ranks, 1..8 */
+    int32_t hidden;           /* H: elements per token, multiple of 8, 8..65536 */
+    int32_t max_tokens;       /* T_max: largest batch (tokens per all-reduce), >= 1 */
+    int32_t reduces_per_step; /* L: all-reduces in one decode step (2 per layer, Sec. 2.4), >= 1 */
+    int32_t validate;         /* SIFAR_VALIDATE_* */
+    int32_t epilogue;         /* 0: plain all-reduce; 1: fused residual-add + RMSNorm */
+    float rms_eps;            /* RMSNorm epsilon (epilogue only) */
+    uint32_t max_attempts;    /* retry budget per chunk (Sec. 4.2's loop is unbounded), >= 1 */
+    uint32_t forced_retries;  /* treat the first k validations as failed (Sec. 6.3 forced-retry measurement) */
+    uint32_t spin_limit;      /* bound on the epilogue's cross-segment wait, in polls, >= 1 */
+    int32_t log_epochs;       /* decision-log ring length, in epochs, >= 1 */
+    int32_t waves_per_group;  /* waves (64 lanes) per workgroup: 1, 2, 4, 8 or 16 */
+} sifar_config;
+
+/* Fills cfg with: N=8, H=4096, T_max=8, L=64, SPEC, no epilogue, eps=1e-6,
+ * max_attempts=1<<20, forced_retries=0, spin_limit=1<<20, log_epochs=64,
+ * waves_per_group=1. Never fails. */
+void sifar_config_default(sifar_config *cfg);
+
+/* Library version: major * 10000 + minor * 100 + patch. */
+int sifar_version(void);
+
+/* Create a handle on the current HIP device. Validates cfg (SIFAR_EINVAL),
+ * allocates the library-owned device state and zeroes it (all stamps 0 =
+ * stale for every epoch g >= 1). *out receives the handle on success, NULL on
+ * failure. */
+int sifar_init(const sifar_config *cfg, sifar_t *out);
+
+/* Release everything the handle owns (synchronises the device first). NULL is a
+ * no-op. */
+void sifar_destroy(sifar_t h);
+
+/* ---- eager calls: one epoch at a time ---------------------------------------
+ * Epochs are numbered from 1. The producer may run at most one epoch ahead of
+ * the reduction: that is all two slots allow (Sec. 3.3); a third produce
+ * before a reduce returns SIFAR_ESTATE. */
+
+/* The emulated peers write epoch g = next produced epoch. Rank r's partial is
+ * read from src + r * src_rank_stride (elements), laid out [tokens][hidden]
+ * bf16, and copied into rank r's slot of parity g & 1; then rank r's stamps of
+ * every chunk are set to g with release semantics (Sec. 4.1: "after the
+ * preceding operation writes its result ... each GPU writes a flag"), except
+ * for ranks the injection table marks late or withheld.
+ * 1 <= tokens <= max_tokens; src_rank_stride >= tokens * hidden, multiple of 8. */
+int sifar_produce(sifar_t h, const void *src, int64_t src_rank_stride, int32_t tokens,
+                  void *stream);
+
+/* Reduce the oldest produced, unreduced epoch into out[tokens][hidden] bf16.
+ * tokens must equal the producer's. Requires epilogue == 0. */
+int sifar_reduce(sifar_t h, void *out, int32_t tokens, void *stream);
+
+/* Reduce the oldest produced epoch and apply the fused epilogue. With a the
+ * all-reduce result rounded to bf16 (not stored):
+ *   residual[t][h] <- bf16( a + residual )                   (in place)
+ *   y[t][h]         = bf16( residual * w[h] / sqrt(mean_h(residual^2) + eps) )
+ * The paper does not describe this epilogue; it is the operation that follows
+ * each all-reduce of a pre-norm transformer layer. residual: [tokens][hidden],
+ * weight: [hidden], y: [tokens][hidden], all bf16. Requires epilogue == 1. */
+int sifar_reduce_rmsnorm(sifar_t h, void *residual, const void *weight, void *y,
+                         int32_t tokens, void *stream);
+
+/* ---- decode step: L chained all-reduces in one captured HIP graph -----------
+ * Binds the caller-owned buffers a step graph uses (Sec. 6.1 times
+ * all-reduces back to back inside the forward pass; Sec. 3.5: a CUDA graph
+ * or megakernel keeps the GPUs in lockstep). Rebinding drops captured graphs.
+ *   src_pool      [pool_entries][N][...] bf16: epoch g's partials are entry
+ *                 (g - 1) % pool_entries; rank r at offset r * pool_rank_stride,
+ *                 [tokens][hidden] inside; entries pool_entry_stride apart.
+ *   out_ring      plain: [L][max_tokens][hidden]; node i writes out_ring[i]
+ *   residual,
+ *   weight, y_ring  epilogue: residual [max_tokens][hidden] (updated in place,
+ *                 chained across the L reduces), weight [hidden], y_ring
+ *                 [L][max_tokens][hidden]; node i writes y_ring[i].
+ * Unused pointers must be NULL. Strides are in elements, multiples of 8. */
+typedef struct {
+    const void *src_pool;
+    int32_t pool_entries;
+    int64_t pool_entry_stride;
+    int64_t pool_rank_stride;
+    void *out_ring;
+    void *residual;
+    const void *weight;
+    void *y_ring;
+} sifar_step_buffers;
+
+int sifar_bind_step(sifar_t h, const sifar_step_buffers *b);
+
+/* Enqueue one decode step for `tokens` tokens: L x (produce, reduce) plus one
+ * epoch-counter advance, as one hipGraphLaunch. The graph for a token count is
+ * captured on first use (on a library-owned stream) and replayed afterwards;
+ * epochs and parities come from a device-resident counter, so a replay needs
+ * no host work. Requires no produced-but-unreduced epoch (SIFAR_ESTATE). */
+int sifar_step(sifar_t h, int32_t tokens, void *stream);
+
+/* ---- injection, logs, state --------------------------------------------------- */
+
+/* Install (copies) a host table of `entries` uint16 words (late | withheld << 8)
+ * for `mode`; SIFAR_INJECT_OFF clears it. Rank bits >= N are ignored. Drops
+ * captured graphs. Not allowed with SIFAR_VALIDATE_NONE. */
+int sifar_set_injection(sifar_t h, const uint16_t *table, int32_t entries, int32_t mode);
+
+/* Decision log geometry: the log is a ring of log_epochs rows of w_max words;
+ * epoch g, chunk c -> word ((g - 1) % log_epochs) * w_max + c. A chunk is the
+ * 512 elements [t][s*512, s*512+512) of token t (the last of a row may be
+ * shorter); c = t * chunks_per_token + s. */
+int sifar_log_geometry(sifar_t h, int32_t *log_epochs, int32_t *chunks_per_token,
+                       int32_t *w_max);
+
+/* Copy the decision log to host memory (synchronises the device). Each word:
+ * bits 0-15 attempts (saturating), 16-23 stale-rank mask of the first
+ * validation, 24-31 stale-rank mask of the last one. `words` must be at most
+ * log_epochs * w_max. */
+int sifar_read_log(sifar_t h, uint32_t *host_dst, size_t words);
+
+/* Next epoch to produce and next epoch to reduce (host-side accounting). */
+int sifar_epochs(sifar_t h, uint32_t *next_produce, uint32_t *next_reduce);
+
+/* Synchronise the device and check the device error word: SIFAR_OK, or
+ * SIFAR_EDEVICE (and the handle is poisoned). */
+int sifar_status(sifar_t h);
+
+/* After SIFAR_EDEVICE: info[0] kind (SIFAR_DEV_*), info[1] epoch, info[2]
+ * chunk, info[3] attempts. Synchronises. */
+int sifar_error_info(sifar_t h, uint32_t info[4]);
+
+/* Static string for a return code. */
+const char *sifar_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SIFAR_H */

@@ -1,0 +1,483 @@
+// Host runtime behind the C ABI of include/sifar.h: configuration checks,
+// library-owned device memory, host-side epoch accounting, eager launches and
+// the captured decode-step graphs.
+#include "sifar.h"
+
+#include <hip/hip_runtime.h>
+
+#include <map>
+#include <new>
+
+#include "sifar_kernels.h"
+
+using namespace sifar;
+
+struct sifar_ctx {
+    sifar_config cfg{};
+    int device = 0;
+    int segs = 0;          // chunks per token
+    int w_max = 0;         // max_tokens * segs
+    int groups_per_token = 1;
+    uint64_t slot_elems = 0;
+
+    uint16_t *slots = nullptr;     // [N][2][slot_elems]
+    uint32_t *stamps = nullptr;    // [2][w_max][N]
+    uint32_t *consumed = nullptr;  // [2][w_max]
+    uint32_t *log = nullptr;       // [log_epochs][w_max]
+    uint64_t *exch = nullptr;      // [max_tokens][groups_per_token]
+    DevState *state = nullptr;
+    uint16_t *inject = nullptr;
+    int32_t inject_entries = 0;
+
+    uint32_t next_prod = 1, next_red = 1;
+    int32_t prod_tokens[2] = {0, 0};
+    uint32_t base_host = 0;        // epoch_base once all enqueued work has run
+    bool poisoned = false;
+
+    bool bound = false;
+    sifar_step_buffers buf{};
+    std::map<int32_t, hipGraphExec_t> graphs;
+    hipStream_t capture = nullptr;
+};
+
+namespace {
+
+constexpr int kVersion = 100;  // 0.1.0
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+template <typename T>
+int dev_alloc(T **p, size_t count) {
+    if (count == 0) count = 1;
+    if (hipMalloc(reinterpret_cast<void **>(p), count * sizeof(T)) != hipSuccess) {
+        *p = nullptr;
+        return SIFAR_ENOMEM;
+    }
+    return SIFAR_OK;
+}
+
+int check_cfg(const sifar_config *c) {
+    if (!c) return SIFAR_EINVAL;
+    if (c->nranks < 1 || c->nranks > kMaxRanks) return SIFAR_EINVAL;
+    if (c->hidden < 8 || c->hidden > 65536 || c->hidden % 8) return SIFAR_EINVAL;
+    if (c->max_tokens < 1 || c->max_tokens > (1 << 20)) return SIFAR_EINVAL;
+    if (c->reduces_per_step < 1 || c->reduces_per_step > (1 << 16)) return SIFAR_EINVAL;
+    if (c->validate < SIFAR_VALIDATE_SPEC || c->validate > SIFAR_VALIDATE_NONE) return SIFAR_EINVAL;
+    if (c->epilogue != 0 && c->epilogue != 1) return SIFAR_EINVAL;
+    if (c->epilogue && !(c->rms_eps >= 0.0f)) return SIFAR_EINVAL;
+    if (c->max_attempts < 1 || c->spin_limit < 1 || c->log_epochs < 1) return SIFAR_EINVAL;
+    const int g = c->waves_per_group;
+    if (g != 1 && g != 2 && g != 4 && g != 8 && g != 16) return SIFAR_EINVAL;
+    return SIFAR_OK;
+}
+
+void drop_graphs(sifar_t h) {
+    for (auto &kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
+    h->graphs.clear();
+}
+
+Geometry geometry(const sifar_t h, int32_t tokens) {
+    Geometry g{};
+    g.nranks = h->cfg.nranks;
+    g.tokens = tokens;
+    g.hidden = h->cfg.hidden;
+    g.segs = h->segs;
+    g.w_max = h->w_max;
+    g.slot_elems = h->slot_elems;
+    return g;
+}
+
+int usable(const sifar_t h) {
+    if (!h) return SIFAR_EINVAL;
+    if (h->poisoned) return SIFAR_ESTATE;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return SIFAR_EHIP;
+    if (dev != h->device) return SIFAR_EINVAL;
+    return SIFAR_OK;
+}
+
+ProduceArgs produce_args(const sifar_t h, int32_t tokens, EpochRef ep, const uint16_t *src,
+                         int64_t entry_stride, int64_t rank_stride, int32_t entries) {
+    ProduceArgs a{};
+    a.geo = geometry(h, tokens);
+    a.ep = ep;
+    a.slots = h->slots;
+    a.stamps = h->stamps;
+    a.consumed = h->consumed;
+    a.src = src;
+    a.entry_stride = entry_stride;
+    a.rank_stride = rank_stride;
+    a.entries = entries;
+    a.inject = h->inject;
+    a.inject_entries = h->inject_entries;
+    a.err = h->state->err;
+    return a;
+}
+
+ReduceArgs reduce_args(const sifar_t h, int32_t tokens, EpochRef ep) {
+    ReduceArgs a{};
+    a.geo = geometry(h, tokens);
+    a.ep = ep;
+    a.slots = h->slots;
+    a.stamps = h->stamps;
+    a.consumed = h->consumed;
+    a.log = h->log;
+    a.log_epochs = h->cfg.log_epochs;
+    a.max_attempts = h->cfg.max_attempts;
+    a.forced_retries = h->cfg.forced_retries;
+    a.spin_limit = h->cfg.spin_limit;
+    a.inject = h->inject;
+    a.inject_entries = h->inject_entries;
+    a.exch = h->exch;
+    a.groups_per_token = h->groups_per_token;
+    a.eps = h->cfg.rms_eps;
+    a.err = h->state->err;
+    return a;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? SIFAR_OK : SIFAR_EHIP; }
+
+int launch_pair(sifar_t h, const ProduceArgs &pa, const ReduceArgs &ra, hipStream_t s) {
+    int rc = hip_status(launch_produce(pa, h->cfg.waves_per_group, s));
+    if (rc) return rc;
+    return hip_status(launch_reduce(ra, h->cfg.validate, h->cfg.epilogue != 0,
+                                    h->cfg.waves_per_group, s));
+}
+
+int capture_step(sifar_t h, int32_t tokens, hipGraphExec_t *out) {
+    const int L = h->cfg.reduces_per_step;
+    const uint32_t advance = static_cast<uint32_t>(L + (L & 1));
+    const uint64_t ring = static_cast<uint64_t>(h->cfg.max_tokens) * h->cfg.hidden;
+    hipStream_t s = h->capture;
+    if (hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal) != hipSuccess) return SIFAR_EHIP;
+    int rc = SIFAR_OK;
+    for (int i = 0; i < L && rc == SIFAR_OK; ++i) {
+        const EpochRef ep{&h->state->epoch_base, static_cast<uint32_t>(i + 1),
+                          static_cast<uint32_t>((i + 1) & 1)};
+        ProduceArgs pa = produce_args(h, tokens, ep, static_cast<const uint16_t *>(h->buf.src_pool),
+                                      h->buf.pool_entry_stride, h->buf.pool_rank_stride,
+                                      h->buf.pool_entries);
+        ReduceArgs ra = reduce_args(h, tokens, ep);
+        if (h->cfg.epilogue) {
+            ra.residual = static_cast<uint16_t *>(h->buf.residual);
+            ra.weight = static_cast<const uint16_t *>(h->buf.weight);
+            ra.y = static_cast<uint16_t *>(h->buf.y_ring) + i * ring;
+        } else {
+            ra.out = static_cast<uint16_t *>(h->buf.out_ring) + i * ring;
+        }
+        rc = launch_pair(h, pa, ra, s);
+    }
+    if (rc == SIFAR_OK) rc = hip_status(launch_advance(&h->state->epoch_base, advance, s));
+    hipGraph_t graph = nullptr;
+    const hipError_t e = hipStreamEndCapture(s, &graph);
+    if (rc == SIFAR_OK && e != hipSuccess) rc = SIFAR_EHIP;
+    if (rc == SIFAR_OK && hipGraphInstantiate(out, graph, nullptr, nullptr, 0) != hipSuccess)
+        rc = SIFAR_EHIP;
+    if (graph) (void)hipGraphDestroy(graph);
+    return rc;
+}
+
+}  // namespace
+
+extern "C" {
+
+void sifar_config_default(sifar_config *c) {
+    if (!c) return;
+    c->nranks = 8;
+    c->hidden = 4096;
+    c->max_tokens = 8;
+    c->reduces_per_step = 64;
+    c->validate = SIFAR_VALIDATE_SPEC;
+    c->epilogue = 0;
+    c->rms_eps = 1e-6f;
+    c->max_attempts = 1u << 20;
+    c->forced_retries = 0;
+    c->spin_limit = 1u << 20;
+    c->log_epochs = 64;
+    c->waves_per_group = 1;
+}
+
+int sifar_version(void) { return kVersion; }
+
+const char *sifar_strerror(int code) {
+    switch (code) {
+        case SIFAR_OK: return "ok";
+        case SIFAR_EINVAL: return "invalid argument";
+        case SIFAR_ENOMEM: return "out of memory";
+        case SIFAR_EHIP: return "HIP runtime error";
+        case SIFAR_ESTATE: return "call out of protocol order, or handle poisoned";
+        case SIFAR_EDEVICE: return "device latched an error";
+    }
+    return "unknown error";
+}
+
+int sifar_init(const sifar_config *cfg, sifar_t *out) {
+    if (!out) return SIFAR_EINVAL;
+    *out = nullptr;
+    int rc = check_cfg(cfg);
+    if (rc) return rc;
+    sifar_t h = new (std::nothrow) sifar_ctx;
+    if (!h) return SIFAR_ENOMEM;
+    h->cfg = *cfg;
+    if (hipGetDevice(&h->device) != hipSuccess) {
+        delete h;
+        return SIFAR_EHIP;
+    }
+    const sifar_config &c = h->cfg;
+    h->segs = (c.hidden + kChunk - 1) / kChunk;
+    h->w_max = c.max_tokens * h->segs;
+    // slots start on 256-byte boundaries
+    h->slot_elems = ((static_cast<uint64_t>(c.max_tokens) * c.hidden + 127) / 128) * 128;
+    if (c.epilogue) {
+        const int G = c.waves_per_group;
+        h->groups_per_token = (h->segs + G - 1) / G;
+        if (h->groups_per_token > kLanes) {
+            delete h;
+            return SIFAR_EINVAL;  // the exchange polls one word per lane
+        }
+        if (h->groups_per_token > 1) {
+            const int cap = max_active_groups(c.nranks, c.validate, true, G);
+            if (cap <= 0 || static_cast<int64_t>(c.max_tokens) * h->groups_per_token > cap) {
+                delete h;
+                return SIFAR_EINVAL;  // a token's groups must be co-resident
+            }
+        }
+    }
+    rc = SIFAR_OK;
+    if (!rc) rc = dev_alloc(&h->slots, static_cast<size_t>(c.nranks) * 2 * h->slot_elems);
+    if (!rc) rc = dev_alloc(&h->stamps, static_cast<size_t>(2) * h->w_max * c.nranks);
+    if (!rc) rc = dev_alloc(&h->consumed, static_cast<size_t>(2) * h->w_max);
+    if (!rc) rc = dev_alloc(&h->log, static_cast<size_t>(c.log_epochs) * h->w_max);
+    if (!rc) rc = dev_alloc(&h->exch, static_cast<size_t>(c.max_tokens) * h->groups_per_token);
+    if (!rc) rc = dev_alloc(&h->state, 1);
+    if (!rc && hipStreamCreateWithFlags(&h->capture, hipStreamNonBlocking) != hipSuccess)
+        rc = SIFAR_EHIP;
+    if (!rc) {
+        hipStream_t s = h->capture;
+        const uint64_t slot_words = static_cast<uint64_t>(c.nranks) * 2 * h->slot_elems / 2;
+        hipError_t e = launch_fill_u32(reinterpret_cast<uint32_t *>(h->slots), 0, slot_words, s);
+        if (e == hipSuccess)
+            e = launch_fill_u32(h->stamps, 0, static_cast<uint64_t>(2) * h->w_max * c.nranks, s);
+        if (e == hipSuccess) e = launch_fill_u32(h->consumed, 0, static_cast<uint64_t>(2) * h->w_max, s);
+        if (e == hipSuccess)
+            e = launch_fill_u32(h->log, 0, static_cast<uint64_t>(c.log_epochs) * h->w_max, s);
+        if (e == hipSuccess)
+            e = launch_fill_u32(reinterpret_cast<uint32_t *>(h->exch), 0,
+                                static_cast<uint64_t>(c.max_tokens) * h->groups_per_token * 2, s);
+        if (e == hipSuccess)
+            e = launch_fill_u32(reinterpret_cast<uint32_t *>(h->state), 0,
+                                sizeof(DevState) / sizeof(uint32_t), s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e != hipSuccess) rc = SIFAR_EHIP;
+    }
+    if (rc) {
+        sifar_destroy(h);
+        return rc;
+    }
+    *out = h;
+    return SIFAR_OK;
+}
+
+void sifar_destroy(sifar_t h) {
+    if (!h) return;
+    (void)hipDeviceSynchronize();
+    drop_graphs(h);
+    if (h->capture) (void)hipStreamDestroy(h->capture);
+    (void)hipFree(h->slots);
+    (void)hipFree(h->stamps);
+    (void)hipFree(h->consumed);
+    (void)hipFree(h->log);
+    (void)hipFree(h->exch);
+    (void)hipFree(h->state);
+    (void)hipFree(h->inject);
+    delete h;
+}
+
+int sifar_produce(sifar_t h, const void *src, int64_t src_rank_stride, int32_t tokens,
+                  void *stream) {
+    int rc = usable(h);
+    if (rc) return rc;
+    if (!src || !aligned16(src) || tokens < 1 || tokens > h->cfg.max_tokens) return SIFAR_EINVAL;
+    if (src_rank_stride % 8 || src_rank_stride < static_cast<int64_t>(tokens) * h->cfg.hidden)
+        return SIFAR_EINVAL;
+    if (h->next_prod - h->next_red > 1) return SIFAR_ESTATE;  // both slots hold unreduced epochs
+    const uint32_t g = h->next_prod;
+    const EpochRef ep{&h->state->zero, g, g & 1u};
+    ProduceArgs pa = produce_args(h, tokens, ep, static_cast<const uint16_t *>(src), 0,
+                                  src_rank_stride, 1);
+    rc = hip_status(launch_produce(pa, h->cfg.waves_per_group, static_cast<hipStream_t>(stream)));
+    if (rc) return rc;
+    h->prod_tokens[g & 1u] = tokens;
+    h->next_prod = g + 1;
+    return SIFAR_OK;
+}
+
+static int reduce_common(sifar_t h, int32_t tokens, void *stream, uint16_t *out, uint16_t *residual,
+                         const uint16_t *weight, uint16_t *y) {
+    const uint32_t g = h->next_red;
+    if (g >= h->next_prod) return SIFAR_ESTATE;  // nothing produced to reduce
+    if (tokens != h->prod_tokens[g & 1u]) return SIFAR_EINVAL;
+    const EpochRef ep{&h->state->zero, g, g & 1u};
+    ReduceArgs ra = reduce_args(h, tokens, ep);
+    ra.out = out;
+    ra.residual = residual;
+    ra.weight = weight;
+    ra.y = y;
+    int rc = hip_status(launch_reduce(ra, h->cfg.validate, h->cfg.epilogue != 0,
+                                      h->cfg.waves_per_group, static_cast<hipStream_t>(stream)));
+    if (rc) return rc;
+    h->next_red = g + 1;
+    return SIFAR_OK;
+}
+
+int sifar_reduce(sifar_t h, void *out, int32_t tokens, void *stream) {
+    int rc = usable(h);
+    if (rc) return rc;
+    if (h->cfg.epilogue) return SIFAR_EINVAL;
+    if (!out || !aligned16(out) || tokens < 1 || tokens > h->cfg.max_tokens) return SIFAR_EINVAL;
+    return reduce_common(h, tokens, stream, static_cast<uint16_t *>(out), nullptr, nullptr, nullptr);
+}
+
+int sifar_reduce_rmsnorm(sifar_t h, void *residual, const void *weight, void *y, int32_t tokens,
+                         void *stream) {
+    int rc = usable(h);
+    if (rc) return rc;
+    if (!h->cfg.epilogue) return SIFAR_EINVAL;
+    if (!residual || !weight || !y || !aligned16(residual) || !aligned16(weight) || !aligned16(y))
+        return SIFAR_EINVAL;
+    if (tokens < 1 || tokens > h->cfg.max_tokens) return SIFAR_EINVAL;
+    return reduce_common(h, tokens, stream, nullptr, static_cast<uint16_t *>(residual),
+                         static_cast<const uint16_t *>(weight), static_cast<uint16_t *>(y));
+}
+
+int sifar_bind_step(sifar_t h, const sifar_step_buffers *b) {
+    int rc = usable(h);
+    if (rc) return rc;
+    if (!b || !b->src_pool || !aligned16(b->src_pool) || b->pool_entries < 1) return SIFAR_EINVAL;
+    const int64_t row = static_cast<int64_t>(h->cfg.max_tokens) * h->cfg.hidden;
+    if (b->pool_rank_stride % 8 || b->pool_entry_stride % 8) return SIFAR_EINVAL;
+    if (b->pool_rank_stride < row) return SIFAR_EINVAL;
+    if (b->pool_entries > 1 && b->pool_entry_stride < b->pool_rank_stride * h->cfg.nranks)
+        return SIFAR_EINVAL;
+    if (h->cfg.epilogue) {
+        if (!b->residual || !b->weight || !b->y_ring || b->out_ring) return SIFAR_EINVAL;
+        if (!aligned16(b->residual) || !aligned16(b->weight) || !aligned16(b->y_ring))
+            return SIFAR_EINVAL;
+    } else {
+        if (!b->out_ring || !aligned16(b->out_ring) || b->residual || b->weight || b->y_ring)
+            return SIFAR_EINVAL;
+    }
+    drop_graphs(h);
+    h->buf = *b;
+    h->bound = true;
+    return SIFAR_OK;
+}
+
+int sifar_step(sifar_t h, int32_t tokens, void *stream) {
+    int rc = usable(h);
+    if (rc) return rc;
+    if (!h->bound) return SIFAR_ESTATE;
+    if (tokens < 1 || tokens > h->cfg.max_tokens) return SIFAR_EINVAL;
+    if (h->next_prod != h->next_red) return SIFAR_ESTATE;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int L = h->cfg.reduces_per_step;
+    // Graph nodes take parity (i + 1) & 1 for epoch base + i + 1: base must be even.
+    uint32_t base = h->next_red - 1;
+    base += base & 1u;
+    auto it = h->graphs.find(tokens);
+    hipGraphExec_t exec = nullptr;
+    if (it == h->graphs.end()) {
+        rc = capture_step(h, tokens, &exec);
+        if (rc) return rc;
+        h->graphs[tokens] = exec;
+    } else {
+        exec = it->second;
+    }
+    if (base != h->base_host) {
+        rc = hip_status(launch_set_base(&h->state->epoch_base, base, s));
+        if (rc) return rc;
+        h->base_host = base;
+    }
+    if (hipGraphLaunch(exec, s) != hipSuccess) return SIFAR_EHIP;
+    h->base_host = base + static_cast<uint32_t>(L + (L & 1));
+    h->next_prod = h->next_red = base + static_cast<uint32_t>(L) + 1;
+    const uint32_t last = h->next_red - 1;
+    h->prod_tokens[last & 1u] = tokens;
+    h->prod_tokens[(last + 1) & 1u] = tokens;
+    return SIFAR_OK;
+}
+
+int sifar_set_injection(sifar_t h, const uint16_t *table, int32_t entries, int32_t mode) {
+    int rc = usable(h);
+    if (rc) return rc;
+    if (mode == SIFAR_INJECT_OFF) {
+        if (hipDeviceSynchronize() != hipSuccess) return SIFAR_EHIP;
+        (void)hipFree(h->inject);
+        h->inject = nullptr;
+        h->inject_entries = 0;
+        drop_graphs(h);
+        return SIFAR_OK;
+    }
+    if (mode != SIFAR_INJECT_DETERMINISTIC) return SIFAR_EINVAL;
+    if (h->cfg.validate == SIFAR_VALIDATE_NONE) return SIFAR_EINVAL;
+    if (!table || entries < 1) return SIFAR_EINVAL;
+    if (hipDeviceSynchronize() != hipSuccess) return SIFAR_EHIP;
+    uint16_t *d = nullptr;
+    rc = dev_alloc(&d, static_cast<size_t>(entries));
+    if (rc) return rc;
+    if (hipMemcpy(d, table, sizeof(uint16_t) * entries, hipMemcpyHostToDevice) != hipSuccess) {
+        (void)hipFree(d);
+        return SIFAR_EHIP;
+    }
+    (void)hipFree(h->inject);
+    h->inject = d;
+    h->inject_entries = entries;
+    drop_graphs(h);
+    return SIFAR_OK;
+}
+
+int sifar_log_geometry(sifar_t h, int32_t *log_epochs, int32_t *chunks_per_token, int32_t *w_max) {
+    if (!h) return SIFAR_EINVAL;
+    if (log_epochs) *log_epochs = h->cfg.log_epochs;
+    if (chunks_per_token) *chunks_per_token = h->segs;
+    if (w_max) *w_max = h->w_max;
+    return SIFAR_OK;
+}
+
+int sifar_read_log(sifar_t h, uint32_t *host_dst, size_t words) {
+    if (!h || !host_dst) return SIFAR_EINVAL;
+    if (words > static_cast<size_t>(h->cfg.log_epochs) * h->w_max) return SIFAR_EINVAL;
+    if (hipDeviceSynchronize() != hipSuccess) return SIFAR_EHIP;
+    if (hipMemcpy(host_dst, h->log, words * sizeof(uint32_t), hipMemcpyDeviceToHost) != hipSuccess)
+        return SIFAR_EHIP;
+    return SIFAR_OK;
+}
+
+int sifar_epochs(sifar_t h, uint32_t *next_produce, uint32_t *next_reduce) {
+    if (!h) return SIFAR_EINVAL;
+    if (next_produce) *next_produce = h->next_prod;
+    if (next_reduce) *next_reduce = h->next_red;
+    return SIFAR_OK;
+}
+
+int sifar_error_info(sifar_t h, uint32_t info[4]) {
+    if (!h || !info) return SIFAR_EINVAL;
+    if (hipDeviceSynchronize() != hipSuccess) return SIFAR_EHIP;
+    if (hipMemcpy(info, h->state->err, 4 * sizeof(uint32_t), hipMemcpyDeviceToHost) != hipSuccess)
+        return SIFAR_EHIP;
+    return SIFAR_OK;
+}
+
+int sifar_status(sifar_t h) {
+    if (!h) return SIFAR_EINVAL;
+    uint32_t info[4] = {0, 0, 0, 0};
+    const int rc = sifar_error_info(h, info);
+    if (rc) return rc;
+    if (info[0] != 0) {
+        h->poisoned = true;
+        return SIFAR_EDEVICE;
+    }
+    return h->poisoned ? SIFAR_ESTATE : SIFAR_OK;
+}
+
+}  // extern "C"

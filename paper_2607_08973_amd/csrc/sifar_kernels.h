@@ -1,0 +1,91 @@
+// Internal interface between the host runtime (api.cpp) and the gfx950
+// kernels (kernels.hip). Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sifar {
+
+constexpr int kLanes = 64;                 // wavefront width on CDNA
+constexpr int kVec = 8;                    // bf16 elements per 16-byte load
+constexpr int kChunk = kLanes * kVec;      // elements per chunk: one wave, one load per rank per lane
+constexpr int kMaxRanks = 8;
+constexpr int kMaxWavesPerGroup = 16;
+
+// Device-resident state shared by all kernels of a handle.
+struct DevState {
+    uint32_t epoch_base;   // graph nodes compute g = epoch_base + node offset
+    uint32_t zero;         // always 0: eager launches pass g as the offset
+    uint32_t err[4];       // kind, epoch, chunk, attempts (first error wins)
+};
+
+// Geometry common to the producer and the reduction.
+struct Geometry {
+    int32_t nranks;
+    int32_t tokens;
+    int32_t hidden;
+    int32_t segs;          // chunks per token = ceil(hidden / kChunk)
+    int32_t w_max;         // max_tokens * segs: stride of the stamp and log rows
+    uint64_t slot_elems;   // elements between consecutive slots
+};
+
+// Where the epoch of a launch comes from: g = *base + off. Parity is frozen at
+// launch (graph capture) time; the host guarantees *base is even for graphs.
+struct EpochRef {
+    const uint32_t *base;
+    uint32_t off;
+    uint32_t parity;
+};
+
+struct ProduceArgs {
+    Geometry geo;
+    EpochRef ep;
+    uint16_t *slots;             // [N][2][slot_elems]
+    uint32_t *stamps;            // [2][w_max][N]
+    const uint32_t *consumed;    // [2][w_max]: last epoch whose reduction finished the chunk
+    const uint16_t *src;         // entry e, rank r: src + e*entry_stride + r*rank_stride
+    int64_t entry_stride;
+    int64_t rank_stride;
+    int32_t entries;             // epoch g uses entry (g - 1) % entries
+    const uint16_t *inject;      // [inject_entries] late | withheld << 8, or null
+    int32_t inject_entries;
+    uint32_t *err;
+};
+
+struct ReduceArgs {
+    Geometry geo;
+    EpochRef ep;
+    const uint16_t *slots;
+    uint32_t *stamps;
+    uint32_t *consumed;
+    uint32_t *log;               // [log_epochs][w_max]
+    int32_t log_epochs;
+    uint32_t max_attempts;
+    uint32_t forced_retries;
+    uint32_t spin_limit;
+    const uint16_t *inject;
+    int32_t inject_entries;
+    uint16_t *out;               // plain: [tokens][hidden]
+    uint16_t *residual;          // epilogue: [tokens][hidden], in place
+    const uint16_t *weight;      // [hidden]
+    uint16_t *y;                 // [tokens][hidden]
+    uint64_t *exch;              // [max_tokens][groups_per_token]: (epoch << 32) | partial bits
+    int32_t groups_per_token;
+    float eps;
+    uint32_t *err;
+};
+
+enum Mode : int { kSpec = 0, kOrdered = 1, kNone = 2 };
+
+hipError_t launch_produce(const ProduceArgs &a, int waves_per_group, hipStream_t s);
+hipError_t launch_reduce(const ReduceArgs &a, int mode, bool epilogue, int waves_per_group,
+                         hipStream_t s);
+// Workgroups of the reduction kernel that can be resident at once on the
+// current device (0 if unknown).
+int max_active_groups(int nranks, int mode, bool epilogue, int waves_per_group);
+hipError_t launch_advance(uint32_t *epoch_base, uint32_t step, hipStream_t s);
+hipError_t launch_set_base(uint32_t *epoch_base, uint32_t value, hipStream_t s);
+hipError_t launch_fill_u32(uint32_t *p, uint32_t value, uint64_t count, hipStream_t s);
+
+}  // namespace sifar

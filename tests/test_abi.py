@@ -1,0 +1,79 @@
+"""The C ABI on a machine without a GPU: the library loads, exports exactly
+what include/sifar.h declares, and rejects bad configurations on the host
+before any device call."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_08973_amd as S
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include",
+                      "sifar.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sifar_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_binding_exports():
+    assert declared_functions() == sorted(S.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = S.load()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_struct_layouts_match_header():
+    # sifar_config: 12 four-byte fields; sifar_step_buffers: pointer/int64 layout
+    assert ctypes.sizeof(S.sifar_config) == 48
+    assert ctypes.sizeof(S.sifar_step_buffers) == 64
+    text = open(HEADER).read()
+    cfg = re.search(r"typedef struct \{([^{}]*)\} sifar_config;", text).group(1)
+    fields = re.findall(r"\b(?:int32_t|uint32_t|float)\s+(\w+);", cfg)
+    assert fields == [f for f, _ in S.sifar_config._fields_]
+    buf = re.search(r"typedef struct \{([^{}]*)\} sifar_step_buffers;", text).group(1)
+    bfields = re.findall(r"\b(\w+);", buf)
+    assert bfields == [f for f, _ in S.sifar_step_buffers._fields_]
+
+
+def test_defaults_and_strings():
+    c = S.sifar_config_default()
+    assert (c.nranks, c.hidden, c.max_tokens, c.reduces_per_step) == (8, 4096, 8, 64)
+    assert c.validate == S.SIFAR_VALIDATE_SPEC and c.epilogue == 0
+    assert abs(c.rms_eps - 1e-6) < 1e-12
+    assert c.max_attempts == 1 << 20 and c.waves_per_group == 1
+    assert S.sifar_version() >= 100
+    for code in (0, -1, -2, -3, -4, -5):
+        assert S.strerror(code)
+    assert S.strerror(-99) == "unknown error"
+
+
+@pytest.mark.parametrize("field,value", [
+    ("nranks", 0), ("nranks", 9), ("hidden", 4), ("hidden", 4100), ("hidden", 65544),
+    ("max_tokens", 0), ("reduces_per_step", 0), ("validate", 3), ("epilogue", 2),
+    ("max_attempts", 0), ("spin_limit", 0), ("log_epochs", 0), ("waves_per_group", 3),
+    ("waves_per_group", 32),
+])
+def test_invalid_config_rejected_on_host(field, value):
+    c = S.sifar_config_default()
+    setattr(c, field, value)
+    h = ctypes.c_void_p()
+    rc = S.load().sifar_init(ctypes.byref(c), ctypes.byref(h))
+    assert rc == S.SIFAR_EINVAL and not h.value
+
+
+def test_null_handle_rejected():
+    L = S.load()
+    assert L.sifar_reduce(None, None, 1, None) == S.SIFAR_EINVAL
+    assert L.sifar_step(None, 1, None) == S.SIFAR_EINVAL
+    assert L.sifar_status(None) == S.SIFAR_EINVAL
+    assert L.sifar_init(None, None) == S.SIFAR_EINVAL
+    L.sifar_destroy(None)

@@ -1,0 +1,323 @@
+"""GPU parity: the HIP path, called through the C ABI, against the CPU oracle.
+
+Bar: every all-reduce output and every residual-stream value bit-exact; the
+RMSNorm output y within 1 bf16 step (the only value behind a reordered
+reduction, the sum of squares over the hidden dimension); every decision-log
+word bit-exact against the protocol simulator's prediction.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_08973_amd as S
+import synth
+from oracle import ref_np, sim
+
+pytestmark = pytest.mark.gpu
+
+from sifar_harness import (DEV, StepRun, expected_log_words, inject_table, to_dev, to_host,
+                           ulp_distance)
+
+ORDERS = {"spec": "spec", "ordered": "ordered"}
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    S.load()  # loud failure if the library is missing
+    yield
+    torch.cuda.synchronize()
+
+
+def _eager_chain(N, T, H, epochs, mode, ahead=False, seed=0, dist="normal"):
+    pool = synth.payload_pool(100 + seed, N, T, H, epochs, dist)
+    src = to_dev(pool)
+    outs = torch.zeros((epochs, T, H), dtype=torch.int16, device=DEV)
+    with S.Sifar(nranks=N, hidden=H, max_tokens=T, reduces_per_step=2, validate=mode,
+                 log_epochs=epochs) as s:
+        if ahead:
+            # the producer runs one epoch ahead: produce g+1 before reducing g
+            s.produce(src[0], T)
+            for g in range(1, epochs + 1):
+                if g < epochs:
+                    s.produce(src[g], T)
+                s.reduce(outs[g - 1], T)
+        else:
+            for g in range(1, epochs + 1):
+                s.produce(src[g - 1], T)
+                s.reduce(outs[g - 1], T)
+        s.check()
+        log = s.read_log()
+    got = to_host(outs)
+    for g in range(epochs):
+        exp = oracle.reduce(pool[g])
+        assert np.array_equal(got[g], exp), f"epoch {g + 1}"
+    return log
+
+
+@pytest.mark.parametrize("mode", ["spec", "ordered", "none"])
+@pytest.mark.parametrize("ahead", [False, True])
+def test_eager_n2_chain64(mode, ahead):
+    """Two ranks, one token of 4096, 64 sequential all-reduces on dual buffers."""
+    log = _eager_chain(2, 1, 4096, 64, mode, ahead)
+    assert np.all(log[:, :8] == sim.pack_log(1, 0, 0))
+
+
+@pytest.mark.parametrize("N", [1, 2, 3, 5, 8])
+@pytest.mark.parametrize("T,H", [(3, 4104), (1, 8), (2, 520), (5, 1000)])
+def test_eager_ragged_shapes(N, T, H):
+    """Several chunks and a ragged last chunk per row; hidden sizes that are not
+    multiples of the 512-element chunk."""
+    _eager_chain(N, T, H, 4, "spec", seed=N * 1000 + H)
+
+
+def test_graph_step_n2_chain64():
+    w = synth.SMOKE_N2
+    run = StepRun(w, 1)
+    epochs = run.step(1)
+    run.s.check()
+    got = to_host(run.out_d)
+    exp = oracle.reduce_chain(run.pool, epochs, 1)
+    for i in range(w.reduces_per_step):
+        assert np.array_equal(got[i, :1], exp[i]), f"node {i}"
+    run.s.close()
+
+
+@pytest.mark.parametrize("mode", ["spec", "ordered", "none"])
+def test_graph_llama_decode_steps(mode):
+    """N=8, batch 1/2/4/8 x 4096, 64 chained all-reduces per decode step."""
+    w = synth.LLAMA8B_DECODE
+    run = StepRun(w, 8, validate=mode)
+    for T in w.tokens:
+        for rep in range(2):
+            epochs = run.step(T)
+            run.s.check()
+            got = to_host(run.out_d)
+            exp = oracle.reduce_chain(run.pool, epochs, T)
+            for i in range(w.reduces_per_step):
+                assert np.array_equal(got[i, :T], exp[i]), f"T={T} rep={rep} node={i}"
+            log = run.s.read_log()
+            assert np.all(log[:, :T * 8] == sim.pack_log(1, 0, 0))
+    run.s.close()
+
+
+def test_graph_llama_full_run_sampled():
+    """The benchmark's configuration: 100 decode steps per batch size, every
+    step replayed from the captured graph; outputs sampled every 9th step."""
+    w = synth.LLAMA8B_DECODE
+    run = StepRun(w, 8)
+    for T in w.tokens:
+        for step in range(w.steps):
+            epochs = run.step(T)
+            if step % 9 == 0 or step == w.steps - 1:
+                got = to_host(run.out_d)
+                for i in range(0, w.reduces_per_step, 7):
+                    g = epochs[i]
+                    exp = oracle.reduce(run.pool[(g - 1) % run.pool.shape[0]][:, :T])
+                    assert np.array_equal(got[i, :T], exp), f"T={T} step={step} node={i}"
+        run.s.check()
+    run.s.close()
+
+
+@pytest.mark.parametrize("order", ["spec", "ordered"])
+@pytest.mark.parametrize("forced", [0, 2])
+def test_stale_injection_deterministic(order, forced):
+    """Speculation stress: each rank's stamp is late with p = 0.1 per epoch;
+    outputs equal the no-speculation oracle and every decision-log word equals
+    the simulator's prediction."""
+    w = synth.SPEC_STRESS
+    steps = 12 if forced == 0 else 4
+    late = synth.delay_table(w.wid, w.nranks, w.reduces_per_step * steps, w.stale_prob)
+    run = StepRun(w, 4, validate=order, forced_retries=forced)
+    run.s.set_injection(inject_table(late))
+    T = 4
+    segs = 8
+    for step in range(steps):
+        epochs = run.step(T)
+        got = to_host(run.out_d)
+        exp = oracle.reduce_chain(run.pool, epochs, T)
+        for i in range(w.reduces_per_step):
+            assert np.array_equal(got[i, :T], exp[i]), f"step={step} node={i}"
+        log = run.s.read_log()
+        masks = [int(late[(g - 1) % len(late)]) for g in epochs]
+        pred = expected_log_words(w.nranks, masks, order, forced)
+        for i, g in enumerate(epochs):
+            row = log[(g - 1) % log.shape[0], :T * segs]
+            assert np.all(row == pred[i]), (step, i, hex(int(row[0])), hex(pred[i]))
+    assert int(np.count_nonzero(late)) > 0
+    run.s.check()
+    run.s.close()
+
+
+def test_withheld_stamp_exhausts_budget():
+    N, T, H = 4, 2, 1024
+    pool = synth.payload_pool(7, N, T, H, 3, "normal")
+    src = to_dev(pool)
+    out = torch.zeros((T, H), dtype=torch.int16, device=DEV)
+    s = S.Sifar(nranks=N, hidden=H, max_tokens=T, reduces_per_step=2, max_attempts=8)
+    s.set_injection(inject_table([0, 0], withheld=[0, 0b0100]))
+    s.produce(src[0], T)
+    s.reduce(out, T)
+    assert s.status() == S.SIFAR_OK
+    s.produce(src[1], T)       # epoch 2: rank 2's stamp never lands
+    s.reduce(out, T)
+    assert s.status() == S.SIFAR_EDEVICE
+    kind, epoch, chunk, attempts = s.error_info()
+    assert (kind, epoch, attempts) == (S.SIFAR_DEV_RETRY_BUDGET, 2, 8)
+    with pytest.raises(S.SifarError):
+        s.produce(src[2], T)   # poisoned
+    s.close()
+
+
+def test_protocol_order_errors():
+    N, T, H = 2, 1, 512
+    pool = synth.payload_pool(8, N, T, H, 4, "normal")
+    src = to_dev(pool)
+    out = torch.zeros((T, H), dtype=torch.int16, device=DEV)
+    with S.Sifar(nranks=N, hidden=H, max_tokens=T, reduces_per_step=2) as s:
+        with pytest.raises(S.SifarError) as e:
+            s.reduce(out, T)                # nothing produced
+        assert e.value.code == S.SIFAR_ESTATE
+        s.produce(src[0], T)
+        s.produce(src[1], T)                # one ahead: allowed
+        with pytest.raises(S.SifarError) as e:
+            s.produce(src[2], T)            # would overwrite epoch 1's slot
+        assert e.value.code == S.SIFAR_ESTATE
+        with pytest.raises(S.SifarError) as e:
+            s.reduce(out, 0)
+        assert e.value.code == S.SIFAR_EINVAL
+        s.reduce(out, T)
+        s.reduce(out, T)
+        with pytest.raises(S.SifarError) as e:
+            s.step(T)                       # nothing bound
+        assert e.value.code == S.SIFAR_ESTATE
+        s.check()
+        assert np.array_equal(to_host(out), oracle.reduce(pool[1]))
+
+
+def test_eager_then_graph_epochs_continue():
+    """Eager epochs, then graph steps: epochs stay unique, parities stay right."""
+    w = synth.Workload(60, "mix", 4, (2,), 2048, 6, 1, "normal")
+    run = StepRun(w, 2)
+    extra = to_dev(synth.payload_pool(61, 4, 2, 2048, 3, "normal"))
+    out = torch.zeros((2, 2048), dtype=torch.int16, device=DEV)
+    for k in range(3):
+        run.s.produce(extra[k], 2)
+        run.s.reduce(out, 2)
+    for rep in range(3):
+        epochs = run.step(2)
+        got = to_host(run.out_d)
+        exp = oracle.reduce_chain(run.pool, epochs, 2)
+        for i in range(6):
+            assert np.array_equal(got[i, :2], exp[i])
+        run.s.produce(extra[rep], 2)
+        run.s.reduce(out, 2)
+        assert np.array_equal(to_host(out), oracle.reduce(synth.payload_pool(61, 4, 2, 2048, 3, "normal")[rep]))
+    run.s.check()
+    run.s.close()
+
+
+def test_pairs_on_gpu_against_oracle():
+    """N=2, H=65536 (the largest row): every bf16 pattern of rank 0 against 256
+    values of rank 1 per reduce, 4 reduces (a sampled slice of all 2^32 pairs,
+    including subnormals, infinities, signed zeros, overflow and ties)."""
+    H, T = 65536, 256
+    a = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    g = np.random.default_rng(23)
+    special = np.array([0x0000, 0x8000, 0x0001, 0x8001, 0x007F, 0x0080, 0x3F80, 0xBF80,
+                        0x7F7F, 0xFF7F, 0x7F80, 0xFF80, 0x3B80, 0xBB80, 0x7B00, 0x7A80], np.uint16)
+    bvals = np.concatenate([special, g.integers(0, 65536, 4 * T - special.size,
+                                                 dtype=np.uint32).astype(np.uint16)])
+    with S.Sifar(nranks=2, hidden=H, max_tokens=T, reduces_per_step=2, log_epochs=4) as s:
+        out = torch.zeros((T, H), dtype=torch.int16, device=DEV)
+        for k in range(4):
+            x = np.empty((2, T, H), np.uint16)
+            x[0] = a[None, :]
+            x[1] = bvals[k * T:(k + 1) * T, None]
+            s.produce(to_dev(x), T)
+            s.reduce(out, T)
+            got = to_host(out)
+            exp = ref_np.reduce(x)
+            fin = ~np.isnan(ref_np.widen(exp))
+            assert np.array_equal(got[fin], exp[fin])
+            assert np.all(np.isnan(ref_np.widen(got[~fin])))
+        s.check()
+
+
+@pytest.mark.parametrize("N,T,H", [(8, 256, 8192), (2, 256, 4096), (4, 64, 8192)])
+def test_payload_sweep_largest_points(N, T, H):
+    """The largest payloads of the latency-to-bandwidth sweep (up to 4 MiB per
+    rank), U(-1, 1) values, full outputs for 3 reduces."""
+    w = synth.Workload(4, f"sweep-n{N}-t{T}-h{H}", N, (T,), H, 4, 1, "uniform")
+    run = StepRun(w, T, pool=synth.payload_pool(4, N, T, H, 5, "uniform"))
+    epochs = run.step(T)
+    got = to_host(run.out_d)
+    for i in range(0, 4):
+        g = epochs[i]
+        assert np.array_equal(got[i], oracle.reduce(run.pool[(g - 1) % 5])), f"node {i}"
+    run.s.check()
+    run.s.close()
+
+
+@pytest.mark.parametrize("waves_per_group", [1, 4, 16])
+@pytest.mark.parametrize("T", [1, 8, 32])
+def test_epilogue_moe_chain(T, waves_per_group):
+    """N=8, hidden 8192, 120 chained all-reduces, each followed by residual-add
+    + RMSNorm, with 5 % late stamps: residual bit-exact at every node, y within
+    1 bf16 step, decision log as predicted."""
+    w = synth.MOE_DECODE
+    steps = 2
+    late = synth.delay_table(w.wid, w.nranks, w.reduces_per_step * steps, w.stale_prob)
+    run = StepRun(w, 32, waves_per_group=waves_per_group)
+    run.s.set_injection(inject_table(late))
+    res = run.res0[:T].copy()
+    segs = 16
+    worst = 0
+    for step in range(steps):
+        res_before = to_host(run.res_d)[:T].copy()
+        assert np.array_equal(res_before, res)
+        epochs = run.step(T)
+        y_got = to_host(run.y_d)
+        a_list, r_list, y_list = oracle.reduce_chain(run.pool, epochs, T,
+                                                     epilogue=(res, run.weight, w.rms_eps))
+        # the residual stream after the last node is on the device
+        assert np.array_equal(to_host(run.res_d)[:T], r_list[-1])
+        for i in range(w.reduces_per_step):
+            d = ulp_distance(y_got[i, :T], y_list[i])
+            worst = max(worst, int(d.max()))
+            assert d.max() <= 1, f"step {step} node {i}: y off by {d.max()} steps"
+        res = r_list[-1]
+        log = run.s.read_log()
+        masks = [int(late[(g - 1) % len(late)]) for g in epochs]
+        pred = expected_log_words(w.nranks, masks, "spec")
+        for i, g in enumerate(epochs):
+            row = log[(g - 1) % log.shape[0], :T * segs]
+            assert np.all(row == pred[i]), (step, i)
+    run.s.check()
+    run.s.close()
+    print(f"epilogue T={T} G={waves_per_group}: max y distance {worst} step(s)")
+
+
+def test_epilogue_residual_chain_every_node_eager():
+    """Eager fused calls: the residual after every node, bit-exact."""
+    N, T, H = 8, 3, 8192
+    pool = synth.payload_pool(55, N, T, H, 5, "act")
+    res0 = synth.residual_init(55, T, H)
+    wgt = synth.rms_weight(55, H)
+    res_d, w_d = to_dev(res0), to_dev(wgt)
+    y = torch.zeros((T, H), dtype=torch.int16, device=DEV)
+    res = res0.copy()
+    with S.Sifar(nranks=N, hidden=H, max_tokens=T, reduces_per_step=2, epilogue=1,
+                 waves_per_group=2) as s:
+        src = to_dev(pool)
+        for g in range(5):
+            s.produce(src[g], T)
+            s.reduce_rmsnorm(res_d, w_d, y, T)
+            a = oracle.reduce(pool[g])
+            res, yy = oracle.residual_rmsnorm(a, res, wgt, float(np.float32(1e-6)))
+            assert np.array_equal(to_host(res_d), res)
+            assert ulp_distance(to_host(y), yy).max() <= 1
+        s.check()
