@@ -1,0 +1,286 @@
+#!/usr/bin/env python3
+"""Benchmark: microseconds per all-reduce of the emulated SiFAR one-shot
+all-reduce on one MI355X, decode-shaped workload of a dense 8B model.
+
+Workload ("llama8b-decode-n8-h4096-chain64"): N = 8 emulated tensor-parallel
+ranks, hidden 4096 bf16, batch 1, 2, 4 and 8 tokens (8-64 KiB per rank), 64
+chained all-reduces per decode step (32 layers x 2). Synthetic activations
+N(0,1)*0.5 with 0.1 % outliers x50, seeded. Inputs are resident in HBM before
+timing starts.
+
+One benchmark step = one captured decode step (64 x produce + reduce, plus
+the epoch advance) for each of the four batch sizes: 256 all-reduces.
+
+Printed JSON line (rank 0):
+  value            microseconds per all-reduce over the timed steps (HIP events
+                   around the graph replays; includes the emulated peers'
+                   writes and every dispatch gap)
+  roofline         the reduction kernel: algorithmic bytes per launch over its
+                   average launch duration, from HIP events around each launch
+                   on the launching stream
+  cpu_baseline     the CPU oracle on this host, on a bounded sample
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+
+
+def reduce_bytes(N: int, T: int, H: int) -> int:
+    """Algorithmic bytes of one all-reduce: read N payloads of T*H bf16, write
+    one result, read N 4-byte stamps per 512-element chunk."""
+    K = T * H * 2
+    chunks = T * ((H + 511) // 512)
+    return N * K + K + 4 * N * chunks
+
+
+def produce_bytes(N: int, T: int, H: int) -> int:
+    """Algorithmic bytes of the emulated peers' write of one epoch: read N
+    partials, write them into the N slots, write N stamps per chunk."""
+    K = T * H * 2
+    chunks = T * ((H + 511) // 512)
+    return 2 * N * K + 4 * N * chunks
+
+
+def graph_floor_us(nodes: int) -> float:
+    """Per-node time of a captured graph of minimal kernels (one-element
+    in-place add): the dispatch floor every launch of a chain pays."""
+    import torch
+
+    x = torch.zeros(1, device="cuda:0")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for _ in range(3):
+            x.add_(1.0)
+    torch.cuda.current_stream().wait_stream(s)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(nodes):
+            x.add_(1.0)
+    for _ in range(3):
+        g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 20
+    a.record()
+    for _ in range(reps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) * 1e3 / (reps * nodes)
+
+
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "fused_reduce_llama8b_decode_n8_h4096.md")
+
+
+def measured_traffic():
+    """HBM bytes per launch of the fused kernel from the committed FETCH_SIZE /
+    WRITE_SIZE profile, or None when the kernel source changed since."""
+    import hashlib
+
+    if not os.path.exists(TRAFFIC_PROFILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_PROFILE):
+        if ":" in line and line.split(":")[0] in ("traffic_bytes_per_launch", "kernels_hip_sha256"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    src = os.path.join(ROOT, "paper_2607_08973_amd", "csrc", "kernels.hip")
+    cur = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    if kv.get("kernels_hip_sha256") != cur or "traffic_bytes_per_launch" not in kv:
+        return None
+    return float(kv["traffic_bytes_per_launch"])
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--mode", default="spec", choices=["spec", "ordered", "none"])
+    ap.add_argument("--fuse", type=int, default=1, choices=[0, 1],
+                    help="1: the peers' next write shares the reduction's launch")
+    ap.add_argument("--floor-nodes", type=int, default=64)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="budget of the CPU-oracle baseline (0 disables it)")
+    return ap.parse_args()
+
+
+def cpu_baseline(pool, tokens, budget_s):
+    """The C oracle, single-threaded, on the same pool entries the GPU reduces."""
+    import numpy as np
+    import oracle
+
+    per_t = {}
+    for T in tokens:
+        xs = [np.ascontiguousarray(pool[e][:, :T]) for e in range(8)]
+        n, t0 = 0, time.perf_counter()
+        while True:
+            oracle.reduce(xs[n % len(xs)])
+            n += 1
+            el = time.perf_counter() - t0
+            if el > budget_s / len(tokens):
+                break
+        per_t[T] = el / n * 1e6
+    mean_us = sum(per_t.values()) / len(per_t)
+    return mean_us, per_t
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build runs on a single MI355X and has no "
+              f"multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2607_08973_amd as S
+    import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    w = synth.LLAMA8B_DECODE
+    N, H, L, tokens = w.nranks, w.hidden, w.reduces_per_step, w.tokens
+    T_max = max(tokens)
+    pool = synth.payload_pool(w.wid, N, T_max, H, w.pool_entries(), w.dist)
+    pool_d = torch.from_numpy(pool.view(np.int16)).to(dev)
+    ring = torch.zeros((L, T_max, H), dtype=torch.int16, device=dev)
+    s = S.Sifar(nranks=N, hidden=H, max_tokens=T_max, reduces_per_step=L, validate=args.mode,
+                log_epochs=L, fuse_peers=args.fuse)
+    s.bind_step(pool_d, out_ring=ring)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        for T in tokens:
+            s.step(T, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    s.check()
+
+    # ---- timed region: K decode steps --------------------------------------
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_total = ev0.elapsed_time(ev1)
+    s.check()
+    reduces = args.steps * len(tokens) * L
+    us_per_reduce = ms_total * 1e3 / reduces
+
+    # per batch size, same method
+    per_t = {}
+    for T in tokens:
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(args.steps):
+            s.step(T, stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        per_t[T] = a.elapsed_time(b) * 1e3 / (args.steps * L)
+    s.check()
+    graph_next_epoch, _ = s.epochs()   # the ring now holds the last step at T = tokens[-1]
+    graph_ring = ring.cpu().numpy().view(np.uint16).copy()
+
+    # ---- dispatch floor: a captured graph of tiny kernels ------------------
+    floor_us = graph_floor_us(args.floor_nodes)
+
+    # ---- roofline of the dominant kernel -----------------------------------
+    # With fused peers a step is produce(g1), L-1 launches of the fused
+    # reduce(g_i)+produce(g_i+1) kernel, reduce(g_L) and the epoch advance:
+    # the fused kernel is L-1 of the L+2 launches. Its average launch period
+    # is the HIP-event step time over the launches of the step.
+    launches = L + 2 if args.fuse else 2 * L + 1
+    kern = {}
+    for T in tokens:
+        period_us = per_t[T] * L / launches
+        byts = reduce_bytes(N, T, H) + (produce_bytes(N, T, H) if args.fuse else 0)
+        kern[T] = {"launch_period_us": period_us, "bytes_per_launch": byts,
+                   "gbs": byts / (period_us * 1e-6) / 1e9}
+    mean_period = sum(k["launch_period_us"] for k in kern.values()) / len(kern)
+    mean_bytes = sum(k["bytes_per_launch"] for k in kern.values()) / len(kern)
+    achieved = mean_bytes / (mean_period * 1e-6) / 1e9
+
+    # ---- parity spot check of the timed graph (outside the timed region) --
+    import oracle
+    T = tokens[-1]
+    for i in (0, L // 2, L - 1):
+        g = graph_next_epoch - L + i
+        exp = oracle.reduce(pool[(g - 1) % pool.shape[0]][:, :T])
+        assert np.array_equal(graph_ring[i, :T], exp), f"graph parity node {i}"
+
+    # ---- calibration copy for hardware byte counters ----------------------
+    # A plain device-to-device copy of exactly 64 MiB: profilers' FETCH_SIZE and
+    # WRITE_SIZE for it give the scale factor between counter units and bytes.
+    calib = torch.empty(64 << 20, dtype=torch.uint8, device=dev)
+    calib_dst = torch.empty_like(calib)
+    calib_dst.copy_(calib)
+    torch.cuda.synchronize()
+    del calib, calib_dst
+
+    traffic = measured_traffic() if (args.fuse and args.mode == "spec") else None
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        cpu_us, cpu_t = cpu_baseline(pool, tokens, args.cpu_seconds)
+        cpu = {"value": round(cpu_us, 3), "unit": "us per all-reduce", "cores": 1,
+               "kind": "oracle",
+               "sample": f"C oracle, 1 thread, the same N=8 x H=4096 pool entries at batch "
+                         f"{list(tokens)} for {args.cpu_seconds:.0f} s total; mean over batch sizes "
+                         f"of per-reduce time: " +
+                         ", ".join(f"T={t}: {v:.1f} us" for t, v in cpu_t.items())}
+
+    s.close()
+    rec = {
+        "metric": "us per all-reduce (N=8, 1-64 tokens x 4096 bf16) + achieved HBM GB/s fraction",
+        "value": round(us_per_reduce, 4),
+        "unit": "us/all-reduce",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_total / args.steps, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 (fp32 accumulate)",
+        "data": "synthetic (seeded N(0,1)*0.5 activations, 0.1% outliers x50)",
+        "config": {"workload": w.name, "nranks": N, "hidden": H, "tokens": list(tokens),
+                   "reduces_per_step": L, "validate": args.mode, "fuse_peers": args.fuse,
+                   "step": f"{len(tokens)} captured decode steps of {L} all-reduces"},
+        "reduces_per_s": round(1e6 / us_per_reduce, 1),
+        "us_per_reduce_by_tokens": {str(k): round(v, 4) for k, v in per_t.items()},
+        "dominant_kernel": {str(k): {kk: (round(vv, 4) if isinstance(vv, float) else vv)
+                                     for kk, vv in v.items()} for k, v in kern.items()},
+        "graph_dispatch_floor_us": round(floor_us, 4),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
+                     "traffic": traffic, "bytes_per_launch": round(mean_bytes),
+                     "launch_period_us": round(mean_period, 4)},
+        "cpu_baseline": cpu,
+        "wall_s_timed": round(wall, 3),
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

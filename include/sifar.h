@@ -113,11 +113,14 @@ typedef struct {
     uint32_t spin_limit;      /* bound on the epilogue's cross-segment wait, in polls, >= 1 */
     int32_t log_epochs;       /* decision-log ring length, in epochs, >= 1 */
     int32_t waves_per_group;  /* waves (64 lanes) per workgroup: 1, 2, 4, 8 or 16 */
+    int32_t fuse_peers;       /* step graphs: 1 = the launch reducing epoch g also writes the
+                                 peers' epoch g + 1 (other parity); 0 = separate producer and
+                                 reduction launches */
 } sifar_config;
 
 /* Fills cfg with: N=8, H=4096, T_max=8, L=64, SPEC, no epilogue, eps=1e-6,
  * max_attempts=1<<20, forced_retries=0, spin_limit=1<<20, log_epochs=64,
- * waves_per_group=1. Never fails. */
+ * waves_per_group=1, fuse_peers=1. Never fails. */
 void sifar_config_default(sifar_config *cfg);
 
 /* Library version: major * 10000 + minor * 100 + patch. */
@@ -188,11 +191,14 @@ typedef struct {
 
 int sifar_bind_step(sifar_t h, const sifar_step_buffers *b);
 
-/* Enqueue one decode step for `tokens` tokens: L x (produce, reduce) plus one
- * epoch-counter advance, as one hipGraphLaunch. The graph for a token count is
- * captured on first use (on a library-owned stream) and replayed afterwards;
- * epochs and parities come from a device-resident counter, so a replay needs
- * no host work. Requires no produced-but-unreduced epoch (SIFAR_ESTATE). */
+/* Enqueue one decode step for `tokens` tokens: L all-reduces plus one
+ * epoch-counter advance, as one hipGraphLaunch. With fuse_peers the graph is
+ * produce(g1), then L-1 launches that each reduce g_i while writing g_(i+1),
+ * then reduce(g_L): L + 1 kernel nodes; without it, L x (produce, reduce).
+ * The graph for a token count is captured on first use (on a library-owned
+ * stream) and replayed afterwards; epochs and parities come from a
+ * device-resident counter, so a replay needs no host work. Requires no
+ * produced-but-unreduced epoch (SIFAR_ESTATE). */
 int sifar_step(sifar_t h, int32_t tokens, void *stream);
 
 /* ---- injection, logs, state --------------------------------------------------- */

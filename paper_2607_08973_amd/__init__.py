@@ -66,6 +66,7 @@ class sifar_config(ctypes.Structure):
         ("spin_limit", ctypes.c_uint32),
         ("log_epochs", ctypes.c_int32),
         ("waves_per_group", ctypes.c_int32),
+        ("fuse_peers", ctypes.c_int32),
     ]
 
 

@@ -68,6 +68,7 @@ int check_cfg(const sifar_config *c) {
     if (c->max_attempts < 1 || c->spin_limit < 1 || c->log_epochs < 1) return SIFAR_EINVAL;
     const int g = c->waves_per_group;
     if (g != 1 && g != 2 && g != 4 && g != 8 && g != 16) return SIFAR_EINVAL;
+    if (c->fuse_peers != 0 && c->fuse_peers != 1) return SIFAR_EINVAL;
     return SIFAR_OK;
 }
 
@@ -137,10 +138,8 @@ ReduceArgs reduce_args(const sifar_t h, int32_t tokens, EpochRef ep) {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? SIFAR_OK : SIFAR_EHIP; }
 
-int launch_pair(sifar_t h, const ProduceArgs &pa, const ReduceArgs &ra, hipStream_t s) {
-    int rc = hip_status(launch_produce(pa, h->cfg.waves_per_group, s));
-    if (rc) return rc;
-    return hip_status(launch_reduce(ra, h->cfg.validate, h->cfg.epilogue != 0,
+int launch_red(sifar_t h, const ReduceArgs &ra, const ProduceArgs *next, hipStream_t s) {
+    return hip_status(launch_reduce(ra, next, h->cfg.validate, h->cfg.epilogue != 0,
                                     h->cfg.waves_per_group, s));
 }
 
@@ -151,21 +150,40 @@ int capture_step(sifar_t h, int32_t tokens, hipGraphExec_t *out) {
     hipStream_t s = h->capture;
     if (hipStreamBeginCapture(s, hipStreamCaptureModeThreadLocal) != hipSuccess) return SIFAR_EHIP;
     int rc = SIFAR_OK;
-    for (int i = 0; i < L && rc == SIFAR_OK; ++i) {
+    auto node_args = [&](int i, ProduceArgs *pa, ReduceArgs *ra) {
         const EpochRef ep{&h->state->epoch_base, static_cast<uint32_t>(i + 1),
                           static_cast<uint32_t>((i + 1) & 1)};
-        ProduceArgs pa = produce_args(h, tokens, ep, static_cast<const uint16_t *>(h->buf.src_pool),
-                                      h->buf.pool_entry_stride, h->buf.pool_rank_stride,
-                                      h->buf.pool_entries);
-        ReduceArgs ra = reduce_args(h, tokens, ep);
+        *pa = produce_args(h, tokens, ep, static_cast<const uint16_t *>(h->buf.src_pool),
+                           h->buf.pool_entry_stride, h->buf.pool_rank_stride, h->buf.pool_entries);
+        *ra = reduce_args(h, tokens, ep);
         if (h->cfg.epilogue) {
-            ra.residual = static_cast<uint16_t *>(h->buf.residual);
-            ra.weight = static_cast<const uint16_t *>(h->buf.weight);
-            ra.y = static_cast<uint16_t *>(h->buf.y_ring) + i * ring;
+            ra->residual = static_cast<uint16_t *>(h->buf.residual);
+            ra->weight = static_cast<const uint16_t *>(h->buf.weight);
+            ra->y = static_cast<uint16_t *>(h->buf.y_ring) + i * ring;
         } else {
-            ra.out = static_cast<uint16_t *>(h->buf.out_ring) + i * ring;
+            ra->out = static_cast<uint16_t *>(h->buf.out_ring) + i * ring;
         }
-        rc = launch_pair(h, pa, ra, s);
+    };
+    ProduceArgs pa{}, pn{};
+    ReduceArgs ra{}, rn{};
+    if (h->cfg.fuse_peers) {
+        node_args(0, &pa, &ra);
+        rc = hip_status(launch_produce(pa, h->cfg.waves_per_group, s));
+        for (int i = 0; i < L && rc == SIFAR_OK; ++i) {
+            node_args(i, &pa, &ra);
+            if (i + 1 < L) {
+                node_args(i + 1, &pn, &rn);
+                rc = launch_red(h, ra, &pn, s);
+            } else {
+                rc = launch_red(h, ra, nullptr, s);
+            }
+        }
+    } else {
+        for (int i = 0; i < L && rc == SIFAR_OK; ++i) {
+            node_args(i, &pa, &ra);
+            rc = hip_status(launch_produce(pa, h->cfg.waves_per_group, s));
+            if (rc == SIFAR_OK) rc = launch_red(h, ra, nullptr, s);
+        }
     }
     if (rc == SIFAR_OK) rc = hip_status(launch_advance(&h->state->epoch_base, advance, s));
     hipGraph_t graph = nullptr;
@@ -195,6 +213,7 @@ void sifar_config_default(sifar_config *c) {
     c->spin_limit = 1u << 20;
     c->log_epochs = 64;
     c->waves_per_group = 1;
+    c->fuse_peers = 1;
 }
 
 int sifar_version(void) { return kVersion; }
@@ -323,8 +342,7 @@ static int reduce_common(sifar_t h, int32_t tokens, void *stream, uint16_t *out,
     ra.residual = residual;
     ra.weight = weight;
     ra.y = y;
-    int rc = hip_status(launch_reduce(ra, h->cfg.validate, h->cfg.epilogue != 0,
-                                      h->cfg.waves_per_group, static_cast<hipStream_t>(stream)));
+    int rc = launch_red(h, ra, nullptr, static_cast<hipStream_t>(stream));
     if (rc) return rc;
     h->next_red = g + 1;
     return SIFAR_OK;

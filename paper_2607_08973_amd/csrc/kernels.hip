@@ -74,46 +74,57 @@ __device__ void latch(uint32_t *err, uint32_t kind, uint32_t g, uint32_t c, uint
 constexpr uint32_t kErrRetryBudget = 1, kErrWaw = 2, kErrExchange = 3;
 
 // ---------------------------------------------------------------------------
-// Producer: the emulated peers. Wave (r, c) copies rank r's part of chunk c
-// into the slot of parity g & 1, then release-stores stamp[p][c][r] = g.
-// Workgroups are numbered chunk-fastest, then token, then rank, the order the
-// reduction numbers its chunks: for a chunk count that is a multiple of the 8
-// XCDs (and one wave per group), the waves writing chunk c run on the XCD
-// that later reduces it.
-__global__ __launch_bounds__(1024) void produce_kernel(ProduceArgs a) {
-    // grid: x = chunk groups of a token, y = token, z = rank
+// Producer: the emulated peers. The wave of chunk c copies every rank's part of
+// the chunk into that rank's slot of parity g & 1, then publishes the N stamps
+// stamp[p][c][r] = g behind one agent-scope release fence (the peers' "write
+// the result, then the flag" of Sec. 4.1). Workgroups are numbered
+// chunk-fastest then token, the order the reduction numbers its chunks, so
+// with one wave per group the producer and the reduction of a chunk run on the
+// same XCD.
+template <int N>
+__device__ __forceinline__ void produce_chunk(const ProduceArgs &a) {
     const int lane = threadIdx.x & (kLanes - 1);
     const Geometry &geo = a.geo;
     const int s = blockIdx.x * (blockDim.x / kLanes) + threadIdx.x / kLanes;
     if (s >= geo.segs) return;
     const int t = blockIdx.y;
-    const int r = blockIdx.z;
     const int c = t * geo.segs + s;
     const uint32_t g = epoch_of(a.ep);
     const uint32_t p = a.ep.parity;
-    const int elem = s * kChunk + lane * kVec;
+    const int elem_raw = s * kChunk + lane * kVec;
+    const bool lane_ok = elem_raw < geo.hidden;
+    const int elem = lane_ok ? elem_raw : geo.hidden - kVec;
+    uint32_t *stamp = a.stamps + (static_cast<size_t>(p) * geo.w_max + c) * N;
 
-    uint32_t *stamp = a.stamps + (static_cast<size_t>(p) * geo.w_max + c) * geo.nranks + r;
-    if (lane == 0) {
-        // Dual-buffer rule: the slot's previous epoch must have been consumed.
-        const uint32_t prev = ld_relaxed(stamp);
-        const uint32_t done = ld_relaxed(a.consumed + static_cast<size_t>(p) * geo.w_max + c);
-        if (prev != done) latch(a.err, kErrWaw, g, c, prev);
+    const uint32_t e = (g - 1u) % static_cast<uint32_t>(a.entries);
+    const uint16_t *src = a.src + e * a.entry_stride + static_cast<int64_t>(t) * geo.hidden + elem;
+    uint16_t *dst = a.slots + static_cast<uint64_t>(p) * geo.slot_elems +
+                    static_cast<uint64_t>(t) * geo.hidden + elem;
+    V16 v[N];
+#pragma unroll
+    for (int r = 0; r < N; ++r) v[r] = ld16(src + r * a.rank_stride);
+    // Dual-buffer rule: each slot's previous epoch must have been consumed.
+    const int rl = lane < N ? lane : N - 1;
+    const uint32_t prev = ld_relaxed(stamp + rl);
+    const uint32_t done = ld_relaxed(a.consumed + static_cast<size_t>(p) * geo.w_max + c);
+    if (lane_ok) {
+#pragma unroll
+        for (int r = 0; r < N; ++r) st16(dst + r * 2 * geo.slot_elems, v[r]);
     }
-    if (elem < geo.hidden) {
-        const uint32_t e = (g - 1u) % static_cast<uint32_t>(a.entries);
-        const uint16_t *src = a.src + e * a.entry_stride + r * a.rank_stride +
-                              static_cast<int64_t>(t) * geo.hidden + elem;
-        uint16_t *dst = a.slots + (static_cast<uint64_t>(r) * 2 + p) * geo.slot_elems +
-                        static_cast<uint64_t>(t) * geo.hidden + elem;
-        st16(dst, ld16(src));
-    }
+    const uint64_t bad = __ballot(lane < N && prev != done);
+    if (bad && lane == __builtin_ctzll(bad)) latch(a.err, kErrWaw, g, c, prev);
+
     uint32_t skip = 0;
-    if (a.inject) {
-        const uint32_t inj = a.inject[(g - 1u) % static_cast<uint32_t>(a.inject_entries)];
-        skip = ((inj | (inj >> 8)) >> r) & 1u;
-    }
-    if (lane == 0 && !skip) st_release(stamp, g);
+    if (a.inject) skip = a.inject[(g - 1u) % static_cast<uint32_t>(a.inject_entries)];
+    skip = (skip | (skip >> 8)) & 0xFFu;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    if (lane < N && !((skip >> lane) & 1u))
+        __hip_atomic_store(stamp + lane, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int N>
+__global__ __launch_bounds__(1024) void produce_kernel(ProduceArgs a) {
+    produce_chunk<N>(a);
 }
 
 // ---------------------------------------------------------------------------
@@ -122,8 +133,16 @@ __global__ __launch_bounds__(1024) void produce_kernel(ProduceArgs a) {
 // store. With EPI the fused residual-add + RMSNorm follows; the token's sum of
 // squares is combined across the waves of the workgroup (LDS) and across the
 // workgroups of the token (epoch-tagged exchange words).
-template <int N, int MODE, bool EPI>
-__global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a) {
+// FUSED: the grid has a second plane (blockIdx.z == 1) of producer workgroups
+// that write the NEXT epoch (other parity) while the first plane reduces this
+// one -- the emulated peers running one epoch ahead, which is as far ahead as
+// two slots allow. The planes touch disjoint slots and stamps.
+template <int N, int MODE, bool EPI, bool FUSED>
+__global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs pa) {
+    if (FUSED && blockIdx.z == 1) {
+        produce_chunk<N>(pa);
+        return;
+    }
     const int lane = threadIdx.x & (kLanes - 1);
     const int wave = threadIdx.x / kLanes;
     const int G = blockDim.x / kLanes;
@@ -314,21 +333,31 @@ __global__ void fill_u32_kernel(uint32_t *p, uint32_t value, uint64_t count) {
 }
 
 template <int N, int MODE>
-hipError_t launch_reduce_nm(const ReduceArgs &a, bool epi, dim3 grid, dim3 block, hipStream_t s) {
-    if (epi)
-        hipLaunchKernelGGL((reduce_kernel<N, MODE, true>), grid, block, 0, s, a);
-    else
-        hipLaunchKernelGGL((reduce_kernel<N, MODE, false>), grid, block, 0, s, a);
+hipError_t launch_reduce_nm(const ReduceArgs &a, const ProduceArgs *pa, bool epi, dim3 grid,
+                            dim3 block, hipStream_t s) {
+    const ProduceArgs none{};
+    if (pa) {
+        grid.z = 2;
+        if (epi)
+            hipLaunchKernelGGL((reduce_kernel<N, MODE, true, true>), grid, block, 0, s, a, *pa);
+        else
+            hipLaunchKernelGGL((reduce_kernel<N, MODE, false, true>), grid, block, 0, s, a, *pa);
+    } else {
+        if (epi)
+            hipLaunchKernelGGL((reduce_kernel<N, MODE, true, false>), grid, block, 0, s, a, none);
+        else
+            hipLaunchKernelGGL((reduce_kernel<N, MODE, false, false>), grid, block, 0, s, a, none);
+    }
     return hipGetLastError();
 }
 
 template <int N>
-hipError_t launch_reduce_n(const ReduceArgs &a, int mode, bool epi, dim3 grid, dim3 block,
-                           hipStream_t s) {
+hipError_t launch_reduce_n(const ReduceArgs &a, const ProduceArgs *pa, int mode, bool epi,
+                           dim3 grid, dim3 block, hipStream_t s) {
     switch (mode) {
-        case kSpec: return launch_reduce_nm<N, kSpec>(a, epi, grid, block, s);
-        case kOrdered: return launch_reduce_nm<N, kOrdered>(a, epi, grid, block, s);
-        case kNone: return launch_reduce_nm<N, kNone>(a, epi, grid, block, s);
+        case kSpec: return launch_reduce_nm<N, kSpec>(a, pa, epi, grid, block, s);
+        case kOrdered: return launch_reduce_nm<N, kOrdered>(a, pa, epi, grid, block, s);
+        case kNone: return launch_reduce_nm<N, kNone>(a, pa, epi, grid, block, s);
     }
     return hipErrorInvalidValue;
 }
@@ -337,25 +366,38 @@ hipError_t launch_reduce_n(const ReduceArgs &a, int mode, bool epi, dim3 grid, d
 
 hipError_t launch_produce(const ProduceArgs &a, int waves_per_group, hipStream_t s) {
     const dim3 grid(static_cast<uint32_t>((a.geo.segs + waves_per_group - 1) / waves_per_group),
-                    static_cast<uint32_t>(a.geo.tokens), static_cast<uint32_t>(a.geo.nranks));
-    hipLaunchKernelGGL(produce_kernel, grid, dim3(waves_per_group * kLanes), 0, s, a);
+                    static_cast<uint32_t>(a.geo.tokens));
+    const dim3 block(waves_per_group * kLanes);
+    switch (a.geo.nranks) {
+        case 1: hipLaunchKernelGGL(produce_kernel<1>, grid, block, 0, s, a); break;
+        case 2: hipLaunchKernelGGL(produce_kernel<2>, grid, block, 0, s, a); break;
+        case 3: hipLaunchKernelGGL(produce_kernel<3>, grid, block, 0, s, a); break;
+        case 4: hipLaunchKernelGGL(produce_kernel<4>, grid, block, 0, s, a); break;
+        case 5: hipLaunchKernelGGL(produce_kernel<5>, grid, block, 0, s, a); break;
+        case 6: hipLaunchKernelGGL(produce_kernel<6>, grid, block, 0, s, a); break;
+        case 7: hipLaunchKernelGGL(produce_kernel<7>, grid, block, 0, s, a); break;
+        case 8: hipLaunchKernelGGL(produce_kernel<8>, grid, block, 0, s, a); break;
+        default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
-hipError_t launch_reduce(const ReduceArgs &a, int mode, bool epilogue, int waves_per_group,
-                         hipStream_t s) {
+hipError_t launch_reduce(const ReduceArgs &a, const ProduceArgs *next, int mode, bool epilogue,
+                         int waves_per_group, hipStream_t s) {
     const dim3 block(waves_per_group * kLanes);
     const dim3 grid(static_cast<uint32_t>((a.geo.segs + waves_per_group - 1) / waves_per_group),
                     static_cast<uint32_t>(a.geo.tokens));
+    if (next && (next->geo.segs != a.geo.segs || next->geo.tokens != a.geo.tokens))
+        return hipErrorInvalidValue;
     switch (a.geo.nranks) {
-        case 1: return launch_reduce_n<1>(a, mode, epilogue, grid, block, s);
-        case 2: return launch_reduce_n<2>(a, mode, epilogue, grid, block, s);
-        case 3: return launch_reduce_n<3>(a, mode, epilogue, grid, block, s);
-        case 4: return launch_reduce_n<4>(a, mode, epilogue, grid, block, s);
-        case 5: return launch_reduce_n<5>(a, mode, epilogue, grid, block, s);
-        case 6: return launch_reduce_n<6>(a, mode, epilogue, grid, block, s);
-        case 7: return launch_reduce_n<7>(a, mode, epilogue, grid, block, s);
-        case 8: return launch_reduce_n<8>(a, mode, epilogue, grid, block, s);
+        case 1: return launch_reduce_n<1>(a, next, mode, epilogue, grid, block, s);
+        case 2: return launch_reduce_n<2>(a, next, mode, epilogue, grid, block, s);
+        case 3: return launch_reduce_n<3>(a, next, mode, epilogue, grid, block, s);
+        case 4: return launch_reduce_n<4>(a, next, mode, epilogue, grid, block, s);
+        case 5: return launch_reduce_n<5>(a, next, mode, epilogue, grid, block, s);
+        case 6: return launch_reduce_n<6>(a, next, mode, epilogue, grid, block, s);
+        case 7: return launch_reduce_n<7>(a, next, mode, epilogue, grid, block, s);
+        case 8: return launch_reduce_n<8>(a, next, mode, epilogue, grid, block, s);
     }
     return hipErrorInvalidValue;
 }
@@ -365,14 +407,14 @@ int max_active_groups(int nranks, int mode, bool epilogue, int waves_per_group) 
 #define SIFAR_PICK(NN)                                                                  \
     if (nranks == NN) {                                                                 \
         if (mode == kSpec)                                                              \
-            fn = epilogue ? (const void *)reduce_kernel<NN, kSpec, true>                \
-                          : (const void *)reduce_kernel<NN, kSpec, false>;              \
+            fn = epilogue ? (const void *)reduce_kernel<NN, kSpec, true, true>          \
+                          : (const void *)reduce_kernel<NN, kSpec, false, false>;       \
         else if (mode == kOrdered)                                                      \
-            fn = epilogue ? (const void *)reduce_kernel<NN, kOrdered, true>             \
-                          : (const void *)reduce_kernel<NN, kOrdered, false>;           \
+            fn = epilogue ? (const void *)reduce_kernel<NN, kOrdered, true, true>       \
+                          : (const void *)reduce_kernel<NN, kOrdered, false, false>;    \
         else                                                                            \
-            fn = epilogue ? (const void *)reduce_kernel<NN, kNone, true>                \
-                          : (const void *)reduce_kernel<NN, kNone, false>;              \
+            fn = epilogue ? (const void *)reduce_kernel<NN, kNone, true, true>          \
+                          : (const void *)reduce_kernel<NN, kNone, false, false>;       \
     }
     SIFAR_PICK(1) SIFAR_PICK(2) SIFAR_PICK(3) SIFAR_PICK(4)
     SIFAR_PICK(5) SIFAR_PICK(6) SIFAR_PICK(7) SIFAR_PICK(8)

@@ -79,8 +79,9 @@ struct ReduceArgs {
 enum Mode : int { kSpec = 0, kOrdered = 1, kNone = 2 };
 
 hipError_t launch_produce(const ProduceArgs &a, int waves_per_group, hipStream_t s);
-hipError_t launch_reduce(const ReduceArgs &a, int mode, bool epilogue, int waves_per_group,
-                         hipStream_t s);
+// With `next` non-null the launch also produces the next epoch (fused peers).
+hipError_t launch_reduce(const ReduceArgs &a, const ProduceArgs *next, int mode, bool epilogue,
+                         int waves_per_group, hipStream_t s);
 // Workgroups of the reduction kernel that can be resident at once on the
 // current device (0 if unknown).
 int max_active_groups(int nranks, int mode, bool epilogue, int waves_per_group);

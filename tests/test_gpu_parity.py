@@ -86,11 +86,12 @@ def test_graph_step_n2_chain64():
     run.s.close()
 
 
+@pytest.mark.parametrize("fuse", [1, 0])
 @pytest.mark.parametrize("mode", ["spec", "ordered", "none"])
-def test_graph_llama_decode_steps(mode):
+def test_graph_llama_decode_steps(mode, fuse):
     """N=8, batch 1/2/4/8 x 4096, 64 chained all-reduces per decode step."""
     w = synth.LLAMA8B_DECODE
-    run = StepRun(w, 8, validate=mode)
+    run = StepRun(w, 8, validate=mode, fuse_peers=fuse)
     for T in w.tokens:
         for rep in range(2):
             epochs = run.step(T)
@@ -122,16 +123,17 @@ def test_graph_llama_full_run_sampled():
     run.s.close()
 
 
+@pytest.mark.parametrize("fuse", [1, 0])
 @pytest.mark.parametrize("order", ["spec", "ordered"])
 @pytest.mark.parametrize("forced", [0, 2])
-def test_stale_injection_deterministic(order, forced):
+def test_stale_injection_deterministic(order, forced, fuse):
     """Speculation stress: each rank's stamp is late with p = 0.1 per epoch;
     outputs equal the no-speculation oracle and every decision-log word equals
     the simulator's prediction."""
     w = synth.SPEC_STRESS
     steps = 12 if forced == 0 else 4
     late = synth.delay_table(w.wid, w.nranks, w.reduces_per_step * steps, w.stale_prob)
-    run = StepRun(w, 4, validate=order, forced_retries=forced)
+    run = StepRun(w, 4, validate=order, forced_retries=forced, fuse_peers=fuse)
     run.s.set_injection(inject_table(late))
     T = 4
     segs = 8
@@ -262,16 +264,17 @@ def test_payload_sweep_largest_points(N, T, H):
     run.s.close()
 
 
+@pytest.mark.parametrize("fuse", [1, 0])
 @pytest.mark.parametrize("waves_per_group", [1, 4, 16])
 @pytest.mark.parametrize("T", [1, 8, 32])
-def test_epilogue_moe_chain(T, waves_per_group):
+def test_epilogue_moe_chain(T, waves_per_group, fuse):
     """N=8, hidden 8192, 120 chained all-reduces, each followed by residual-add
     + RMSNorm, with 5 % late stamps: residual bit-exact at every node, y within
     1 bf16 step, decision log as predicted."""
     w = synth.MOE_DECODE
     steps = 2
     late = synth.delay_table(w.wid, w.nranks, w.reduces_per_step * steps, w.stale_prob)
-    run = StepRun(w, 32, waves_per_group=waves_per_group)
+    run = StepRun(w, 32, waves_per_group=waves_per_group, fuse_peers=fuse)
     run.s.set_injection(inject_table(late))
     res = run.res0[:T].copy()
     segs = 16
