@@ -111,6 +111,10 @@ def parse():
     ap.add_argument("--fuse", type=int, default=1, choices=[0, 1],
                     help="1: the peers' next write shares the reduction's launch")
     ap.add_argument("--floor-nodes", type=int, default=64)
+    ap.add_argument("--workload", default="llama8b-decode",
+                    choices=["llama8b-decode", "smoke-n2", "spec-stress", "sweep", "moe-rmsnorm"],
+                    help="llama8b-decode is the headline line; the others print one "
+                         "JSON line per configuration")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline (0 disables it)")
     return ap.parse_args()
@@ -136,12 +140,138 @@ def cpu_baseline(pool, tokens, budget_s):
     return mean_us, per_t
 
 
+def time_steps(s, T, steps, stream):
+    """HIP-event time of `steps` replays of the step graph for T tokens (ms)."""
+    import torch
+
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record(stream)
+    for _ in range(steps):
+        s.step(T, stream)
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b)
+
+
+def chain_point(w, T, args, *, T_max=None, pool_entries=None, inject=False, waves_per_group=1,
+                check_nodes=(0, -1)):
+    """Measure one captured chain configuration. Returns a JSON-ready dict."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2607_08973_amd as S
+    import synth
+    from oracle import sim
+
+    dev = "cuda:0"
+    N, H, L = w.nranks, w.hidden, w.reduces_per_step
+    T_max = T_max or T
+    P = pool_entries or w.pool_entries()
+    pool = synth.payload_pool(w.wid, N, T_max, H, P, w.dist)
+    pool_d = torch.from_numpy(pool.view(np.int16)).to(dev)
+    stream = torch.cuda.current_stream()
+    s = S.Sifar(nranks=N, hidden=H, max_tokens=T_max, reduces_per_step=L, validate=args.mode,
+                log_epochs=L, fuse_peers=args.fuse, epilogue=int(w.epilogue),
+                rms_eps=w.rms_eps, waves_per_group=waves_per_group)
+    if w.epilogue:
+        res0 = synth.residual_init(w.wid, T_max, H)
+        wgt = synth.rms_weight(w.wid, H)
+        res_d = torch.from_numpy(res0.view(np.int16)).to(dev)
+        w_d = torch.from_numpy(wgt.view(np.int16)).to(dev)
+        ring = torch.zeros((L, T_max, H), dtype=torch.int16, device=dev)
+        s.bind_step(pool_d, residual=res_d, weight=w_d, y_ring=ring)
+    else:
+        ring = torch.zeros((L, T_max, H), dtype=torch.int16, device=dev)
+        s.bind_step(pool_d, out_ring=ring)
+    late = None
+    if inject and w.stale_prob > 0:
+        E = L * (args.warmup + args.steps + 1)
+        late = synth.delay_table(w.wid, N, E, w.stale_prob)
+        s.set_injection([int(x) for x in late])
+    for _ in range(args.warmup):
+        s.step(T, stream)
+    torch.cuda.synchronize()
+    s.check()
+    ms = time_steps(s, T, args.steps, stream)
+    s.check()
+    nxt, _ = s.epochs()
+    epochs = list(range(nxt - L, nxt))
+    out = {"workload": w.name, "nranks": N, "tokens": T, "hidden": H, "chain": L,
+           "steps": args.steps, "us_per_reduce": ms * 1e3 / (args.steps * L)}
+    launches = L + 2 if args.fuse else 2 * L + 1
+    out["launch_period_us"] = ms * 1e3 / (args.steps * launches)
+    K = T * H * 2
+    red = reduce_bytes(N, T, H) + (3 * K + 2 * H if w.epilogue else 0)
+    out["reduce_bytes"] = red
+    out["reduce_gbs"] = red / (out["us_per_reduce"] * 1e-6) / 1e9
+    fused = red + (produce_bytes(N, T, H) if args.fuse else 0)
+    out["launch_bytes"] = fused
+    out["launch_gbs"] = fused / (out["launch_period_us"] * 1e-6) / 1e9
+    # parity spot check of the last replay (outside the timed region)
+    got = ring.cpu().numpy().view(np.uint16)
+    if not w.epilogue:
+        for i in check_nodes:
+            g = epochs[i]
+            exp = oracle.reduce(pool[(g - 1) % P][:, :T])
+            assert np.array_equal(got[i, :T], exp), f"{w.name} T={T} node {i}"
+    log = s.read_log()
+    segs = (H + 511) // 512
+    rows = np.array([log[(g - 1) % L, :T * segs] for g in epochs])
+    att = rows & 0xFFFF
+    out["chunks_retried_frac"] = float(np.mean(att > 1))
+    out["mean_attempts"] = float(np.mean(att))
+    if late is not None:
+        masks = [int(late[(g - 1) % len(late)]) for g in epochs]
+        pred = sim.predict_log(N, masks, args.mode)
+        assert all(np.all(rows[i] == pred[i]) for i in range(L)), "decision log != prediction"
+        out["epochs_with_late_stamp_frac"] = float(np.mean([m != 0 for m in masks]))
+        out["log_matches_prediction"] = True
+    s.close()
+    return out
+
+
+def suite(args):
+    """Secondary workloads: one JSON line each (not the headline metric)."""
+    import synth
+
+    if args.workload == "smoke-n2":
+        pts = [chain_point(synth.SMOKE_N2, 1, args)]
+    elif args.workload == "spec-stress":
+        pts = [chain_point(synth.SPEC_STRESS, 4, args, inject=True),
+               chain_point(synth.SPEC_STRESS, 4, args, inject=False)]
+    elif args.workload == "sweep":
+        pts = [chain_point(w, w.tokens[0], args, pool_entries=5) for w in synth.PAYLOAD_SWEEP]
+    elif args.workload == "moe-rmsnorm":
+        w = synth.MOE_DECODE
+        pts = []
+        for T in w.tokens:
+            for G in (1, 4, 16):
+                p = chain_point(w, T, args, T_max=max(w.tokens), inject=True, waves_per_group=G)
+                p["waves_per_group"] = G
+                pts.append(p)
+    else:
+        raise SystemExit(f"unknown workload {args.workload}")
+    for p in pts:
+        p["validate"] = args.mode
+        p["fuse_peers"] = args.fuse
+        print(json.dumps({k: (round(v, 4) if isinstance(v, float) else v) for k, v in p.items()}),
+              flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build runs on a single MI355X and has no "
               f"multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
+    if args.workload != "llama8b-decode":
+        import torch
+
+        assert torch.cuda.is_available(), "bench.py needs a GPU"
+        suite(args)
+        return
 
     import numpy as np
     import torch
