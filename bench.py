@@ -110,6 +110,9 @@ def parse():
     ap.add_argument("--mode", default="spec", choices=["spec", "ordered", "none"])
     ap.add_argument("--fuse", type=int, default=1, choices=[0, 1],
                     help="1: the peers' next write shares the reduction's launch")
+    ap.add_argument("--persistent", type=int, default=1, choices=[0, 1],
+                    help="1: one persistent launch per decode step (peers and reduction "
+                         "concurrent); 0: one launch per all-reduce")
     ap.add_argument("--floor-nodes", type=int, default=64)
     ap.add_argument("--workload", default="llama8b-decode",
                     choices=["llama8b-decode", "smoke-n2", "spec-stress", "sweep", "moe-rmsnorm"],
@@ -169,12 +172,19 @@ def chain_point(w, T, args, *, T_max=None, pool_entries=None, inject=False, wave
     N, H, L = w.nranks, w.hidden, w.reduces_per_step
     T_max = T_max or T
     P = pool_entries or w.pool_entries()
+    stream = torch.cuda.current_stream()
+    try:
+        s = S.Sifar(nranks=N, hidden=H, max_tokens=T_max, reduces_per_step=L,
+                    validate=args.mode, log_epochs=L, fuse_peers=args.fuse,
+                    epilogue=int(w.epilogue), rms_eps=w.rms_eps,
+                    waves_per_group=waves_per_group, persistent=args.persistent)
+    except S.SifarError as err:
+        if args.persistent and err.code == S.SIFAR_EINVAL:
+            return {"workload": w.name, "nranks": N, "tokens": T, "hidden": H, "chain": L,
+                    "skipped": "persistent step needs more co-resident waves than the GPU holds"}
+        raise
     pool = synth.payload_pool(w.wid, N, T_max, H, P, w.dist)
     pool_d = torch.from_numpy(pool.view(np.int16)).to(dev)
-    stream = torch.cuda.current_stream()
-    s = S.Sifar(nranks=N, hidden=H, max_tokens=T_max, reduces_per_step=L, validate=args.mode,
-                log_epochs=L, fuse_peers=args.fuse, epilogue=int(w.epilogue),
-                rms_eps=w.rms_eps, waves_per_group=waves_per_group)
     if w.epilogue:
         res0 = synth.residual_init(w.wid, T_max, H)
         wgt = synth.rms_weight(w.wid, H)
@@ -200,13 +210,15 @@ def chain_point(w, T, args, *, T_max=None, pool_entries=None, inject=False, wave
     epochs = list(range(nxt - L, nxt))
     out = {"workload": w.name, "nranks": N, "tokens": T, "hidden": H, "chain": L,
            "steps": args.steps, "us_per_reduce": ms * 1e3 / (args.steps * L)}
-    launches = L + 2 if args.fuse else 2 * L + 1
+    launches = 1 if args.persistent else (L + 2 if args.fuse else 2 * L + 1)
     out["launch_period_us"] = ms * 1e3 / (args.steps * launches)
     K = T * H * 2
     red = reduce_bytes(N, T, H) + (3 * K + 2 * H if w.epilogue else 0)
     out["reduce_bytes"] = red
     out["reduce_gbs"] = red / (out["us_per_reduce"] * 1e-6) / 1e9
-    fused = red + (produce_bytes(N, T, H) if args.fuse else 0)
+    fused = red + (produce_bytes(N, T, H) if (args.fuse or args.persistent) else 0)
+    if args.persistent:
+        fused *= L
     out["launch_bytes"] = fused
     out["launch_gbs"] = fused / (out["launch_period_us"] * 1e-6) / 1e9
     # parity spot check of the last replay (outside the timed region)
@@ -222,12 +234,15 @@ def chain_point(w, T, args, *, T_max=None, pool_entries=None, inject=False, wave
     att = rows & 0xFFFF
     out["chunks_retried_frac"] = float(np.mean(att > 1))
     out["mean_attempts"] = float(np.mean(att))
+    assert np.all((rows >> 24) == 0), "a chunk was accepted with a stale stamp"
     if late is not None:
         masks = [int(late[(g - 1) % len(late)]) for g in epochs]
-        pred = sim.predict_log(N, masks, args.mode)
-        assert all(np.all(rows[i] == pred[i]) for i in range(L)), "decision log != prediction"
         out["epochs_with_late_stamp_frac"] = float(np.mean([m != 0 for m in masks]))
-        out["log_matches_prediction"] = True
+        if not args.persistent:
+            # launches in stream order: every decision is predictable exactly
+            pred = sim.predict_log(N, masks, args.mode)
+            assert all(np.all(rows[i] == pred[i]) for i in range(L)), "decision log != prediction"
+            out["log_matches_prediction"] = True
     s.close()
     return out
 
@@ -254,8 +269,12 @@ def suite(args):
     else:
         raise SystemExit(f"unknown workload {args.workload}")
     for p in pts:
+        if "skipped" in p:
+            print(json.dumps(p), flush=True)
+            continue
         p["validate"] = args.mode
         p["fuse_peers"] = args.fuse
+        p["persistent"] = args.persistent
         print(json.dumps({k: (round(v, 4) if isinstance(v, float) else v) for k, v in p.items()}),
               flush=True)
 
@@ -289,7 +308,7 @@ def main():
     pool_d = torch.from_numpy(pool.view(np.int16)).to(dev)
     ring = torch.zeros((L, T_max, H), dtype=torch.int16, device=dev)
     s = S.Sifar(nranks=N, hidden=H, max_tokens=T_max, reduces_per_step=L, validate=args.mode,
-                log_epochs=L, fuse_peers=args.fuse)
+                log_epochs=L, fuse_peers=args.fuse, persistent=args.persistent)
     s.bind_step(pool_d, out_ring=ring)
     stream = torch.cuda.current_stream()
 
@@ -340,11 +359,15 @@ def main():
     # reduce(g_i)+produce(g_i+1) kernel, reduce(g_L) and the epoch advance:
     # the fused kernel is L-1 of the L+2 launches. Its average launch period
     # is the HIP-event step time over the launches of the step.
-    launches = L + 2 if args.fuse else 2 * L + 1
+    if args.persistent:
+        launches, per_launch = 1, L
+    else:
+        launches, per_launch = (L + 2 if args.fuse else 2 * L + 1), 1
     kern = {}
     for T in tokens:
         period_us = per_t[T] * L / launches
-        byts = reduce_bytes(N, T, H) + (produce_bytes(N, T, H) if args.fuse else 0)
+        byts = per_launch * (reduce_bytes(N, T, H) +
+                             (produce_bytes(N, T, H) if (args.fuse or args.persistent) else 0))
         kern[T] = {"launch_period_us": period_us, "bytes_per_launch": byts,
                    "gbs": byts / (period_us * 1e-6) / 1e9}
     mean_period = sum(k["launch_period_us"] for k in kern.values()) / len(kern)
@@ -368,7 +391,8 @@ def main():
     torch.cuda.synchronize()
     del calib, calib_dst
 
-    traffic = measured_traffic() if (args.fuse and args.mode == "spec") else None
+    traffic = (measured_traffic() if (args.fuse and args.mode == "spec" and not args.persistent)
+               else None)
 
     cpu = None
     if args.cpu_seconds > 0:
@@ -396,6 +420,7 @@ def main():
         "data": "synthetic (seeded N(0,1)*0.5 activations, 0.1% outliers x50)",
         "config": {"workload": w.name, "nranks": N, "hidden": H, "tokens": list(tokens),
                    "reduces_per_step": L, "validate": args.mode, "fuse_peers": args.fuse,
+                   "persistent": args.persistent,
                    "step": f"{len(tokens)} captured decode steps of {L} all-reduces"},
         "reduces_per_s": round(1e6 / us_per_reduce, 1),
         "us_per_reduce_by_tokens": {str(k): round(v, 4) for k, v in per_t.items()},

@@ -116,11 +116,17 @@ typedef struct {
     int32_t fuse_peers;       /* step graphs: 1 = the launch reducing epoch g also writes the
                                  peers' epoch g + 1 (other parity); 0 = separate producer and
                                  reduction launches */
+    int32_t persistent;       /* step graphs: 1 = one persistent launch runs the whole step, its
+                                 consumer waves and the emulated peers' waves synchronising
+                                 through stamps in flight (a megakernel-style chain, Sec. 5);
+                                 needs 2 x max_tokens x ceil(hidden / 512) co-resident waves */
+    uint32_t late_delay;      /* persistent steps with injection: a late rank's stamp lands
+                                 this many ~0.2 us sleeps after its payload */
 } sifar_config;
 
 /* Fills cfg with: N=8, H=4096, T_max=8, L=64, SPEC, no epilogue, eps=1e-6,
  * max_attempts=1<<20, forced_retries=0, spin_limit=1<<20, log_epochs=64,
- * waves_per_group=1, fuse_peers=1. Never fails. */
+ * waves_per_group=1, fuse_peers=1, persistent=0, late_delay=8. Never fails. */
 void sifar_config_default(sifar_config *cfg);
 
 /* Library version: major * 10000 + minor * 100 + patch. */
@@ -194,7 +200,11 @@ int sifar_bind_step(sifar_t h, const sifar_step_buffers *b);
 /* Enqueue one decode step for `tokens` tokens: L all-reduces plus one
  * epoch-counter advance, as one hipGraphLaunch. With fuse_peers the graph is
  * produce(g1), then L-1 launches that each reduce g_i while writing g_(i+1),
- * then reduce(g_L): L + 1 kernel nodes; without it, L x (produce, reduce).
+ * then reduce(g_L): L + 1 kernel nodes; without it, L x (produce, reduce);
+ * with persistent, one launch for the whole step. In a persistent step the
+ * peers run concurrently with the reduction, so mis-speculation happens for
+ * real (the decision log records it) and injected late stamps land after
+ * late_delay instead of after the first failed validation.
  * The graph for a token count is captured on first use (on a library-owned
  * stream) and replayed afterwards; epochs and parities come from a
  * device-resident counter, so a replay needs no host work. Requires no

@@ -67,6 +67,8 @@ class sifar_config(ctypes.Structure):
         ("log_epochs", ctypes.c_int32),
         ("waves_per_group", ctypes.c_int32),
         ("fuse_peers", ctypes.c_int32),
+        ("persistent", ctypes.c_int32),
+        ("late_delay", ctypes.c_uint32),
     ]
 
 

@@ -23,8 +23,10 @@ struct sifar_ctx {
     uint16_t *slots = nullptr;     // [N][2][slot_elems]
     uint32_t *stamps = nullptr;    // [2][w_max][N]
     uint32_t *consumed = nullptr;  // [2][w_max]
+    uint32_t *produced = nullptr;  // [2][w_max]
     uint32_t *log = nullptr;       // [log_epochs][w_max]
-    uint64_t *exch = nullptr;      // [max_tokens][groups_per_token]
+    uint64_t *exch = nullptr;      // [2][max_tokens][exch_q]
+    int exch_q = 1;                // exchange words per token and parity
     DevState *state = nullptr;
     uint16_t *inject = nullptr;
     int32_t inject_entries = 0;
@@ -69,6 +71,7 @@ int check_cfg(const sifar_config *c) {
     const int g = c->waves_per_group;
     if (g != 1 && g != 2 && g != 4 && g != 8 && g != 16) return SIFAR_EINVAL;
     if (c->fuse_peers != 0 && c->fuse_peers != 1) return SIFAR_EINVAL;
+    if (c->persistent != 0 && c->persistent != 1) return SIFAR_EINVAL;
     return SIFAR_OK;
 }
 
@@ -105,6 +108,7 @@ ProduceArgs produce_args(const sifar_t h, int32_t tokens, EpochRef ep, const uin
     a.slots = h->slots;
     a.stamps = h->stamps;
     a.consumed = h->consumed;
+    a.produced = h->produced;
     a.src = src;
     a.entry_stride = entry_stride;
     a.rank_stride = rank_stride;
@@ -131,6 +135,7 @@ ReduceArgs reduce_args(const sifar_t h, int32_t tokens, EpochRef ep) {
     a.inject_entries = h->inject_entries;
     a.exch = h->exch;
     a.groups_per_token = h->groups_per_token;
+    a.exch_parity_stride = h->cfg.max_tokens * h->exch_q;
     a.eps = h->cfg.rms_eps;
     a.err = h->state->err;
     return a;
@@ -166,7 +171,20 @@ int capture_step(sifar_t h, int32_t tokens, hipGraphExec_t *out) {
     };
     ProduceArgs pa{}, pn{};
     ReduceArgs ra{}, rn{};
-    if (h->cfg.fuse_peers) {
+    if (h->cfg.persistent) {
+        ChainArgs ca{};
+        node_args(0, &ca.p, &ca.r);
+        ca.r.ep.off = 0;  // the chain derives every epoch from the base itself
+        ca.p.ep.off = 0;
+        ca.r.groups_per_token = h->segs;  // one wave per workgroup
+        ca.reduces = L;
+        ca.ring_stride = ring;
+        ca.late_delay = h->cfg.late_delay;
+        ca.epoch_base = &h->state->epoch_base;
+        ca.advance = advance;
+        ca.done = &h->state->chain_done;
+        rc = hip_status(launch_chain(ca, h->cfg.validate, h->cfg.epilogue != 0, s));
+    } else if (h->cfg.fuse_peers) {
         node_args(0, &pa, &ra);
         rc = hip_status(launch_produce(pa, h->cfg.waves_per_group, s));
         for (int i = 0; i < L && rc == SIFAR_OK; ++i) {
@@ -185,7 +203,8 @@ int capture_step(sifar_t h, int32_t tokens, hipGraphExec_t *out) {
             if (rc == SIFAR_OK) rc = launch_red(h, ra, nullptr, s);
         }
     }
-    if (rc == SIFAR_OK) rc = hip_status(launch_advance(&h->state->epoch_base, advance, s));
+    if (rc == SIFAR_OK && !h->cfg.persistent)  // the persistent launch advances it itself
+        rc = hip_status(launch_advance(&h->state->epoch_base, advance, s));
     hipGraph_t graph = nullptr;
     const hipError_t e = hipStreamEndCapture(s, &graph);
     if (rc == SIFAR_OK && e != hipSuccess) rc = SIFAR_EHIP;
@@ -214,6 +233,8 @@ void sifar_config_default(sifar_config *c) {
     c->log_epochs = 64;
     c->waves_per_group = 1;
     c->fuse_peers = 1;
+    c->persistent = 0;
+    c->late_delay = 8;
 }
 
 int sifar_version(void) { return kVersion; }
@@ -250,7 +271,7 @@ int sifar_init(const sifar_config *cfg, sifar_t *out) {
     if (c.epilogue) {
         const int G = c.waves_per_group;
         h->groups_per_token = (h->segs + G - 1) / G;
-        if (h->groups_per_token > kLanes) {
+        if (h->groups_per_token > kLanes || (c.persistent && h->segs > kLanes)) {
             delete h;
             return SIFAR_EINVAL;  // the exchange polls one word per lane
         }
@@ -262,12 +283,22 @@ int sifar_init(const sifar_config *cfg, sifar_t *out) {
             }
         }
     }
+    h->exch_q = c.persistent && h->segs > h->groups_per_token ? h->segs : h->groups_per_token;
+    if (c.persistent) {
+        // every consumer and producer wave of a step is resident at once
+        const int cap = max_active_chain_groups(c.nranks, c.validate, c.epilogue != 0);
+        if (cap <= 0 || 2 * static_cast<int64_t>(h->w_max) > cap) {
+            delete h;
+            return SIFAR_EINVAL;
+        }
+    }
     rc = SIFAR_OK;
     if (!rc) rc = dev_alloc(&h->slots, static_cast<size_t>(c.nranks) * 2 * h->slot_elems);
     if (!rc) rc = dev_alloc(&h->stamps, static_cast<size_t>(2) * h->w_max * c.nranks);
     if (!rc) rc = dev_alloc(&h->consumed, static_cast<size_t>(2) * h->w_max);
+    if (!rc) rc = dev_alloc(&h->produced, static_cast<size_t>(2) * h->w_max);
     if (!rc) rc = dev_alloc(&h->log, static_cast<size_t>(c.log_epochs) * h->w_max);
-    if (!rc) rc = dev_alloc(&h->exch, static_cast<size_t>(c.max_tokens) * h->groups_per_token);
+    if (!rc) rc = dev_alloc(&h->exch, static_cast<size_t>(2) * c.max_tokens * h->exch_q);
     if (!rc) rc = dev_alloc(&h->state, 1);
     if (!rc && hipStreamCreateWithFlags(&h->capture, hipStreamNonBlocking) != hipSuccess)
         rc = SIFAR_EHIP;
@@ -278,11 +309,12 @@ int sifar_init(const sifar_config *cfg, sifar_t *out) {
         if (e == hipSuccess)
             e = launch_fill_u32(h->stamps, 0, static_cast<uint64_t>(2) * h->w_max * c.nranks, s);
         if (e == hipSuccess) e = launch_fill_u32(h->consumed, 0, static_cast<uint64_t>(2) * h->w_max, s);
+        if (e == hipSuccess) e = launch_fill_u32(h->produced, 0, static_cast<uint64_t>(2) * h->w_max, s);
         if (e == hipSuccess)
             e = launch_fill_u32(h->log, 0, static_cast<uint64_t>(c.log_epochs) * h->w_max, s);
         if (e == hipSuccess)
             e = launch_fill_u32(reinterpret_cast<uint32_t *>(h->exch), 0,
-                                static_cast<uint64_t>(c.max_tokens) * h->groups_per_token * 2, s);
+                                static_cast<uint64_t>(2) * c.max_tokens * h->exch_q * 2, s);
         if (e == hipSuccess)
             e = launch_fill_u32(reinterpret_cast<uint32_t *>(h->state), 0,
                                 sizeof(DevState) / sizeof(uint32_t), s);
@@ -305,6 +337,7 @@ void sifar_destroy(sifar_t h) {
     (void)hipFree(h->slots);
     (void)hipFree(h->stamps);
     (void)hipFree(h->consumed);
+    (void)hipFree(h->produced);
     (void)hipFree(h->log);
     (void)hipFree(h->exch);
     (void)hipFree(h->state);

@@ -4,17 +4,26 @@
 // token's row, handled by one 64-lane wave with one 16-byte load per rank per
 // lane. Every chunk carries its own N epoch stamps (the paper's per-threadblock
 // validation buffer, Sec. 4.2), so chunks validate and retry independently and
-// no wave ever waits for another during the reduction proper.
+// no wave waits for another during the reduction proper.
 //
-// Memory-model choices (LLVM AMDGPU memory model for GFX942/950):
-//  - stamps are read with agent-scope atomic loads (coherent across the XCDs'
-//    separate L2s); the producer stores them after its payload stores, and the
-//    end of the producing launch publishes both device-wide;
+// Two ways to run a decode step:
+//  - per-epoch launches (eager calls, step graphs): the producer of an epoch
+//    always finishes in an earlier launch than the reduction of that epoch;
+//  - one persistent launch per step (chain_kernel): consumer and producer
+//    waves run concurrently and synchronise through stamps and per-chunk
+//    consumed/produced words, with agent-scope release/acquire.
+//
+// Memory-model choices (LLVM AMDGPU memory model for GFX942/950; the 8 XCDs
+// have separate L2s, so agent scope means "coherent across XCDs"):
+//  - stamps are read with agent-scope atomic loads;
 //  - SPEC issues the payload loads and the stamp loads together, with no
 //    ordering between them (the paper's concurrent payload warps and
 //    validation warp); ORDERED acquires the stamps before loading the payload;
 //  - a retry starts with an acquire fence so the reloads cannot be served
-//    from a stale cache line (the paper's L1-bypassing re-read, Sec. 4.2).
+//    from a stale cache line (the paper's L1-bypassing re-read, Sec. 4.2);
+//  - in the persistent chain the payload is read with agent-scope loads too
+//    (no stale L2 line from the slot's previous use), and the producer
+//    publishes with one agent-scope release fence per wave and epoch.
 //
 // Arithmetic: fp32 adds in ascending rank order (no reassociation, no FMA
 // contraction), bf16 rounding by the native V_CVT_PK_BF16_F32 (round to nearest
@@ -30,6 +39,19 @@ struct alignas(16) V16 {
 
 __device__ __forceinline__ V16 ld16(const uint16_t *p) {
     return *reinterpret_cast<const V16 *>(p);
+}
+
+// 16 bytes as two agent-scope atomic loads: coherent across the XCDs' L2s.
+__device__ __forceinline__ V16 ld16_agent(const uint16_t *p) {
+    const uint64_t *q = reinterpret_cast<const uint64_t *>(p);
+    const uint64_t a = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t b = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    V16 v;
+    v.w[0] = static_cast<uint32_t>(a);
+    v.w[1] = static_cast<uint32_t>(a >> 32);
+    v.w[2] = static_cast<uint32_t>(b);
+    v.w[3] = static_cast<uint32_t>(b >> 32);
+    return v;
 }
 
 __device__ __forceinline__ void st16(uint16_t *p, const V16 &v) {
@@ -54,8 +76,19 @@ __device__ __forceinline__ uint32_t ld_acquire(const uint32_t *p) {
     return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+__device__ __forceinline__ void st_relaxed(uint32_t *p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ __forceinline__ void st_release(uint32_t *p, uint32_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Makes every load that fed `v` complete before any later instruction issues:
+// the value is consumed by an (empty) compiler barrier, so the compiler must
+// wait for it there.
+__device__ __forceinline__ void complete(const V16 &v) {
+    asm volatile("" ::"v"(v.w[0]), "v"(v.w[1]), "v"(v.w[2]), "v"(v.w[3]) : "memory");
 }
 
 __device__ __forceinline__ uint32_t epoch_of(const EpochRef &e) { return e.base[0] + e.off; }
@@ -65,70 +98,104 @@ __device__ void latch(uint32_t *err, uint32_t kind, uint32_t g, uint32_t c, uint
     uint32_t expected = 0;
     if (__hip_atomic_compare_exchange_strong(err, &expected, kind, __ATOMIC_RELAXED,
                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
-        __hip_atomic_store(err + 1, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(err + 2, c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(err + 3, n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        st_relaxed(err + 1, g);
+        st_relaxed(err + 2, c);
+        st_relaxed(err + 3, n);
     }
 }
 
+__device__ __forceinline__ bool latched(const uint32_t *err) { return ld_relaxed(err) != 0; }
+
 constexpr uint32_t kErrRetryBudget = 1, kErrWaw = 2, kErrExchange = 3;
 
+// Where the calling lane works: token t, chunk s of the row, chunk index c.
+// Lanes past the end of the row load a clamped, in-bounds address and do not
+// store (lane_ok false); waves past the last chunk are inactive.
+struct Chunk {
+    int t, s, c;
+    bool active, lane_ok;
+    int elem;
+    uint64_t row;
+};
+
+__device__ __forceinline__ Chunk chunk_at(const Geometry &geo, int t, int s, int lane) {
+    Chunk k;
+    k.t = t;
+    k.active = s < geo.segs;
+    k.s = k.active ? s : geo.segs - 1;
+    k.c = t * geo.segs + k.s;
+    const int raw = s * kChunk + lane * kVec;
+    k.lane_ok = k.active && raw < geo.hidden;
+    const int e = k.s * kChunk + lane * kVec;
+    k.elem = e < geo.hidden ? e : geo.hidden - kVec;
+    k.row = static_cast<uint64_t>(t) * geo.hidden + k.elem;
+    return k;
+}
+
+__device__ __forceinline__ uint32_t log_word(uint32_t attempts, uint32_t first, uint32_t last) {
+    return (attempts > 0xFFFFu ? 0xFFFFu : attempts) | ((first & 0xFFu) << 16) |
+           ((last & 0xFFu) << 24);
+}
+
 // ---------------------------------------------------------------------------
-// Producer: the emulated peers. The wave of chunk c copies every rank's part of
-// the chunk into that rank's slot of parity g & 1, then stores the N stamps
-// stamp[p][c][r] = g (the peers' "write the result, then the flag" of
-// Sec. 4.1). The stamp stores are ordered after the payload stores of the wave
-// (workgroup-scope release). Device-wide visibility comes from the end of the
-// launch: the reduction of an epoch always runs in a later launch than its
-// producer (eagerly, in a step graph, and in the fused plane, which writes the
-// epoch after the one its launch reduces), and the end-of-kernel release makes
-// every store of a launch visible to all XCDs before the next launch starts --
-// as in the paper, where the flag follows the preceding kernel's completion.
-// An agent-scope release fence here would write back the XCD's whole L2 once
-// per wave; measured on MI355X it costs ~0.1-0.2 us of XCD-serialised time per
-// fence and caps the 38 MB all-reduce at 0.9 TB/s instead of 5.7 TB/s.
-// Workgroups are numbered chunk-fastest then token, the order the reduction
-// numbers its chunks, so with one wave per group the producer and the
-// reduction of a chunk run on the same XCD.
+// Producer side: the emulated peers.
+
+// Copy every rank's part of chunk k of epoch g into the slots of parity p.
+template <int N>
+__device__ __forceinline__ void copy_chunk(const ProduceArgs &a, const Chunk &k, uint32_t g,
+                                           uint32_t p) {
+    const Geometry &geo = a.geo;
+    const uint32_t e = (g - 1u) % static_cast<uint32_t>(a.entries);
+    const uint16_t *src = a.src + e * a.entry_stride + static_cast<int64_t>(k.row);
+    uint16_t *dst = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + k.row;
+    V16 v[N];
+#pragma unroll
+    for (int r = 0; r < N; ++r) v[r] = ld16(src + r * a.rank_stride);
+    if (k.lane_ok) {
+#pragma unroll
+        for (int r = 0; r < N; ++r) st16(dst + r * 2 * geo.slot_elems, v[r]);
+    }
+}
+
+// Ranks whose stamp the injection table holds back at epoch g (late | withheld).
+__device__ __forceinline__ uint32_t held_back(const uint16_t *inject, int32_t entries, uint32_t g) {
+    if (!inject) return 0;
+    const uint32_t inj = inject[(g - 1u) % static_cast<uint32_t>(entries)];
+    return (inj | (inj >> 8)) & 0xFFu;
+}
+
+// Producer of one epoch in its own launch (eager calls, step graphs). The
+// stamp stores are ordered after the payload stores of the wave
+// (workgroup-scope release); device-wide visibility comes from the end of the
+// launch, because the reduction of an epoch always runs in a later launch than
+// its producer (eagerly, in a step graph, and in the fused plane, which writes
+// the epoch after the one its launch reduces) -- as in the paper, whose flag
+// follows the preceding kernel's completion (Sec. 4.2). An agent-scope release
+// here would write back the XCD's whole L2 once per wave; measured on MI355X
+// that costs ~0.1-0.2 us of XCD-serialised time per fence and caps a 38 MB
+// all-reduce at 0.9 TB/s instead of 5.7 TB/s. Workgroups are numbered
+// chunk-fastest then token, the order the reduction numbers its chunks, so with
+// one wave per group the producer and the reduction of a chunk share an XCD.
 template <int N>
 __device__ __forceinline__ void produce_chunk(const ProduceArgs &a) {
     const int lane = threadIdx.x & (kLanes - 1);
     const Geometry &geo = a.geo;
-    const int s = blockIdx.x * (blockDim.x / kLanes) + threadIdx.x / kLanes;
-    if (s >= geo.segs) return;
-    const int t = blockIdx.y;
-    const int c = t * geo.segs + s;
+    const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x * (blockDim.x / kLanes) +
+                                                  threadIdx.x / kLanes, lane);
+    if (!k.active) return;
     const uint32_t g = epoch_of(a.ep);
     const uint32_t p = a.ep.parity;
-    const int elem_raw = s * kChunk + lane * kVec;
-    const bool lane_ok = elem_raw < geo.hidden;
-    const int elem = lane_ok ? elem_raw : geo.hidden - kVec;
-    uint32_t *stamp = a.stamps + (static_cast<size_t>(p) * geo.w_max + c) * N;
-
-    const uint32_t e = (g - 1u) % static_cast<uint32_t>(a.entries);
-    const uint16_t *src = a.src + e * a.entry_stride + static_cast<int64_t>(t) * geo.hidden + elem;
-    uint16_t *dst = a.slots + static_cast<uint64_t>(p) * geo.slot_elems +
-                    static_cast<uint64_t>(t) * geo.hidden + elem;
-    V16 v[N];
-#pragma unroll
-    for (int r = 0; r < N; ++r) v[r] = ld16(src + r * a.rank_stride);
-    // Dual-buffer rule: each slot's previous epoch must have been consumed.
-    const int rl = lane < N ? lane : N - 1;
-    const uint32_t prev = ld_relaxed(stamp + rl);
-    const uint32_t done = ld_relaxed(a.consumed + static_cast<size_t>(p) * geo.w_max + c);
-    if (lane_ok) {
-#pragma unroll
-        for (int r = 0; r < N; ++r) st16(dst + r * 2 * geo.slot_elems, v[r]);
-    }
-    const uint64_t bad = __ballot(lane < N && prev != done);
-    if (bad && lane == __builtin_ctzll(bad)) latch(a.err, kErrWaw, g, c, prev);
-
-    uint32_t skip = 0;
-    if (a.inject) skip = a.inject[(g - 1u) % static_cast<uint32_t>(a.inject_entries)];
-    skip = (skip | (skip >> 8)) & 0xFFu;
+    const size_t pc = static_cast<size_t>(p) * geo.w_max + k.c;
+    // Dual-buffer rule: the slot's previous epoch must have been consumed.
+    const uint32_t prev = ld_relaxed(a.produced + pc);
+    const uint32_t done = ld_relaxed(a.consumed + pc);
+    copy_chunk<N>(a, k, g, p);
+    if (lane == 0 && prev != done) latch(a.err, kErrWaw, g, k.c, prev);
+    const uint32_t held = held_back(a.inject, a.inject_entries, g);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    if (lane < N && !((skip >> lane) & 1u))
-        __hip_atomic_store(stamp + lane, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t *stamp = a.stamps + pc * N;
+    if (lane < N && !((held >> lane) & 1u)) st_relaxed(stamp + lane, g);
+    if (lane == 0) st_relaxed(a.produced + pc, g);
 }
 
 template <int N>
@@ -137,86 +204,67 @@ __global__ __launch_bounds__(1024) void produce_kernel(ProduceArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Reduction of one chunk per wave: speculative or ordered loads, per-rank
-// stamp validation by ballot, bounded retry, fp32 sum in rank order, bf16
-// store. With EPI the fused residual-add + RMSNorm follows; the token's sum of
-// squares is combined across the waves of the workgroup (LDS) and across the
-// workgroups of the token (epoch-tagged exchange words).
-// FUSED: the grid has a second plane (blockIdx.z == 1) of producer workgroups
-// that write the NEXT epoch (other parity) while the first plane reduces this
-// one -- the emulated peers running one epoch ahead, which is as far ahead as
-// two slots allow. The planes touch disjoint slots and stamps.
-template <int N, int MODE, bool EPI, bool FUSED>
-__global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs pa) {
-    if (FUSED && blockIdx.z == 1) {
-        produce_chunk<N>(pa);
-        return;
-    }
-    const int lane = threadIdx.x & (kLanes - 1);
-    const int wave = threadIdx.x / kLanes;
-    const int G = blockDim.x / kLanes;
+// Consumer side.
+
+template <int N, bool AGENT>
+__device__ __forceinline__ void load_payload(V16 (&v)[N], const uint16_t *slot0, uint64_t rank_step) {
+#pragma unroll
+    for (int r = 0; r < N; ++r) v[r] = AGENT ? ld16_agent(slot0 + r * rank_step)
+                                             : ld16(slot0 + r * rank_step);
+}
+
+// Load chunk k of epoch g, validate its N stamps, retry while any is stale.
+// AGENT: payload through agent-scope loads (persistent chain), stamps first.
+// INJECT_HOOK: deterministic injection, the late ranks' stamps land right
+// after the first failed validation (only when producers have finished).
+template <int N, int MODE, bool AGENT, bool INJECT_HOOK>
+__device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint32_t g, uint32_t p,
+                                       int lane, V16 (&v)[N], uint32_t &attempts, uint32_t &first,
+                                       uint32_t &last) {
     const Geometry &geo = a.geo;
-
-    // grid: x = chunk groups of a token, y = token
-    const int t = blockIdx.y;
-    const int s = blockIdx.x * G + wave;
-    if (!EPI && s >= geo.segs) return;
-    // EPI: trailing waves of a token's last group idle but join the barriers;
-    // every lane loads in bounds (clamped) and only lane_ok lanes store.
-    const bool active = s < geo.segs;
-    const int sc = active ? s : geo.segs - 1;
-    const int c = t * geo.segs + sc;
-    const int elem_raw = s * kChunk + lane * kVec;
-    const bool lane_ok = active && elem_raw < geo.hidden;
-    const int elem = sc * kChunk + lane * kVec < geo.hidden ? sc * kChunk + lane * kVec
-                                                            : geo.hidden - kVec;
-    const uint32_t p = a.ep.parity;
-    const uint64_t row = static_cast<uint64_t>(t) * geo.hidden + elem;
-
-    const uint16_t *slot0 = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + row;
+    const uint16_t *slot0 = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + k.row;
     const uint64_t rank_step = 2 * geo.slot_elems;  // slots are [rank][parity]
-    uint32_t *stamp = a.stamps + (static_cast<size_t>(p) * geo.w_max + c) * N;
-
-    V16 v[N];
-    V16 rv, wv;
-    if (EPI) {
-        rv = ld16(a.residual + row);
-        wv = ld16(a.weight + elem);
-    }
-    const uint32_t g = epoch_of(a.ep);
+    uint32_t *stamp = a.stamps + (static_cast<size_t>(p) * geo.w_max + k.c) * N;
 
     uint32_t st = 0;
     if (MODE == kOrdered) {
-        if (active && lane < N) st = ld_acquire(stamp + lane);
+        if (k.active && lane < N) st = ld_acquire(stamp + lane);
+    } else if (AGENT) {
+        if (MODE == kSpec && k.active && lane < N) st = ld_relaxed(stamp + lane);
+        load_payload<N, AGENT>(v, slot0, rank_step);
     } else {
-#pragma unroll
-        for (int r = 0; r < N; ++r) v[r] = ld16(slot0 + r * rank_step);
-        if (MODE == kSpec && active && lane < N) st = ld_relaxed(stamp + lane);
+        load_payload<N, AGENT>(v, slot0, rank_step);
+        if (MODE == kSpec && k.active && lane < N) st = ld_relaxed(stamp + lane);
     }
 
-    uint32_t attempts = 1, first = 0, last = 0;
-    if (MODE != kNone && active) {
+    attempts = 1;
+    first = last = 0;
+    if (MODE != kNone && k.active) {
         uint32_t m = static_cast<uint32_t>(__ballot(lane < N && st != g));
         first = last = m;
         bool fail = m != 0 || a.forced_retries >= 1;
         while (fail) {
             if (attempts >= a.max_attempts) {
-                if (lane == 0) latch(a.err, kErrRetryBudget, g, c, attempts);
+                if (lane == 0) latch(a.err, kErrRetryBudget, g, k.c, attempts);
                 break;
             }
-            if (attempts == 1 && a.inject && m != 0) {
-                // Deterministic injection: the late ranks catch up right now.
+            if (INJECT_HOOK && attempts == 1 && a.inject && m != 0) {
                 const uint32_t inj = a.inject[(g - 1u) % static_cast<uint32_t>(a.inject_entries)];
                 if (lane < N && ((inj >> lane) & 1u) && !((inj >> (8 + lane)) & 1u))
                     st_release(stamp + lane, g);
             }
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            if (AGENT && m != 0) {
+                if (latched(a.err)) break;  // the step is already failing: stop waiting
+                __builtin_amdgcn_s_sleep(1);  // a live peer is still writing
+            }
+            // Plain reloads need an acquire fence (an L2 invalidate) to see the
+            // peers' data; agent-scope reloads are coherent without one.
+            if (!AGENT) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             if (MODE == kOrdered) {
                 if (lane < N) st = ld_acquire(stamp + lane);
             } else {
                 if (lane < N) st = ld_relaxed(stamp + lane);
-#pragma unroll
-                for (int r = 0; r < N; ++r) v[r] = ld16(slot0 + r * rank_step);
+                load_payload<N, AGENT>(v, slot0, rank_step);
             }
             ++attempts;
             m = static_cast<uint32_t>(__ballot(lane < N && st != g));
@@ -224,12 +272,12 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
             fail = m != 0 || attempts <= a.forced_retries;
         }
     }
-    if (MODE == kOrdered) {
-#pragma unroll
-        for (int r = 0; r < N; ++r) v[r] = ld16(slot0 + r * rank_step);
-    }
+    if (MODE == kOrdered) load_payload<N, AGENT>(v, slot0, rank_step);
+}
 
-    // Fixed-order fp32 sum: acc = x_0; acc += x_1; ... acc += x_{N-1}.
+// Fixed-order fp32 sum: acc = x_0; acc += x_1; ... acc += x_{N-1}; then bf16.
+template <int N>
+__device__ __forceinline__ V16 sum_round(const V16 (&v)[N]) {
     float acc[kVec];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -247,37 +295,40 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
     V16 o;
 #pragma unroll
     for (int k = 0; k < 4; ++k) o.w[k] = pack_bf16(acc[2 * k], acc[2 * k + 1]);
+    return o;
+}
 
-    if (active && lane == 0) {
-        const uint32_t word = (attempts > 0xFFFFu ? 0xFFFFu : attempts) | ((first & 0xFFu) << 16) |
-                              ((last & 0xFFu) << 24);
-        a.log[static_cast<size_t>((g - 1u) % static_cast<uint32_t>(a.log_epochs)) * geo.w_max + c] =
-            word;
-        a.consumed[static_cast<size_t>(p) * geo.w_max + c] = g;
-    }
+__device__ __forceinline__ void write_log(const ReduceArgs &a, const Chunk &k, uint32_t g,
+                                          uint32_t word) {
+    a.log[static_cast<size_t>((g - 1u) % static_cast<uint32_t>(a.log_epochs)) * a.geo.w_max + k.c] =
+        word;
+}
 
-    if (!EPI) {
-        if (lane_ok) st16(a.out + row, o);
-        return;
-    }
-
-    // ---- fused residual-add + RMSNorm -------------------------------------
+// Residual-add + RMSNorm of one chunk after its all-reduce result o. The
+// token's sum of squares is combined across the waves of the workgroup (LDS)
+// and across the token's Q workgroups (epoch-tagged exchange words, double
+// buffered by parity). Every wave of the workgroup must call this.
+__device__ __forceinline__ void residual_rmsnorm(const ReduceArgs &a, const Chunk &k, uint32_t g,
+                                                 uint32_t p, const V16 &o, const V16 &rv,
+                                                 const V16 &wv, uint16_t *y, int lane, int wave,
+                                                 int G, int q) {
+    const Geometry &geo = a.geo;
     // res' = bf16(a + res), with a = the bf16 all-reduce result.
     V16 nr;
     float x[kVec];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const float a0 = lo_f32(o.w[k]), a1 = hi_f32(o.w[k]);
-        nr.w[k] = pack_bf16(a0 + lo_f32(rv.w[k]), a1 + hi_f32(rv.w[k]));
-        x[2 * k] = lo_f32(nr.w[k]);
-        x[2 * k + 1] = hi_f32(nr.w[k]);
+    for (int i = 0; i < 4; ++i) {
+        const float a0 = lo_f32(o.w[i]), a1 = hi_f32(o.w[i]);
+        nr.w[i] = pack_bf16(a0 + lo_f32(rv.w[i]), a1 + hi_f32(rv.w[i]));
+        x[2 * i] = lo_f32(nr.w[i]);
+        x[2 * i + 1] = hi_f32(nr.w[i]);
     }
-    if (lane_ok) st16(a.residual + row, nr);
+    if (k.lane_ok) st16(a.residual + k.row, nr);
 
     float ss = 0.f;
-    if (lane_ok) {
+    if (k.lane_ok) {
 #pragma unroll
-        for (int k = 0; k < kVec; ++k) ss = __builtin_fmaf(x[k], x[k], ss);
+        for (int i = 0; i < kVec; ++i) ss = __builtin_fmaf(x[i], x[i], ss);
     }
     // Butterfly: every lane ends with the bit-identical wave total.
 #pragma unroll
@@ -293,8 +344,8 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
     const int Q = a.groups_per_token;
     if (Q > 1) {
         if (wave == 0) {
-            const int q = blockIdx.x;
-            uint64_t *ex = a.exch + static_cast<size_t>(t) * Q;
+            uint64_t *ex = a.exch + static_cast<size_t>(p) * a.exch_parity_stride +
+                           static_cast<size_t>(k.t) * Q;
             if (lane == 0) {
                 const uint64_t word = (static_cast<uint64_t>(g) << 32) | __float_as_uint(grp);
                 __hip_atomic_store(ex + q, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -307,7 +358,7 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
                     mine = __hip_atomic_load(ex + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 ready = __ballot(lane < Q && static_cast<uint32_t>(mine >> 32) != g) == 0;
             } while (!ready && ++spins < a.spin_limit);
-            if (!ready && lane == 0) latch(a.err, kErrExchange, g, c, spins);
+            if (!ready && lane == 0) latch(a.err, kErrExchange, g, k.c, spins);
             const float pv = __uint_as_float(static_cast<uint32_t>(mine));
             float tot = 0.f;
             for (int j = 0; j < Q; ++j) tot = tot + __shfl(pv, j);
@@ -320,11 +371,165 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
     const float inv = 1.0f / __builtin_sqrtf(grp / static_cast<float>(geo.hidden) + a.eps);
     V16 yo;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const float w0 = lo_f32(wv.w[k]), w1 = hi_f32(wv.w[k]);
-        yo.w[k] = pack_bf16((x[2 * k] * inv) * w0, (x[2 * k + 1] * inv) * w1);
+    for (int i = 0; i < 4; ++i) {
+        const float w0 = lo_f32(wv.w[i]), w1 = hi_f32(wv.w[i]);
+        yo.w[i] = pack_bf16((x[2 * i] * inv) * w0, (x[2 * i + 1] * inv) * w1);
     }
-    if (lane_ok) st16(a.y + row, yo);
+    if (k.lane_ok) st16(y + k.row, yo);
+}
+
+// ---------------------------------------------------------------------------
+// Reduction of one epoch, one chunk per wave: speculative or ordered loads,
+// per-rank stamp validation by ballot, bounded retry, fp32 sum in rank order,
+// bf16 store, optional fused epilogue.
+// FUSED: the grid has a second plane (blockIdx.z == 1) of producer workgroups
+// that write the NEXT epoch (other parity) while the first plane reduces this
+// one -- the emulated peers running one epoch ahead, which is as far ahead as
+// two slots allow. The planes touch disjoint slots and stamps.
+template <int N, int MODE, bool EPI, bool FUSED>
+__global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs pa) {
+    if (FUSED && blockIdx.z == 1) {
+        produce_chunk<N>(pa);
+        return;
+    }
+    const int lane = threadIdx.x & (kLanes - 1);
+    const int wave = threadIdx.x / kLanes;
+    const int G = blockDim.x / kLanes;
+    const Geometry &geo = a.geo;
+    // grid: x = chunk groups of a token, y = token
+    const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x * G + wave, lane);
+    if (!EPI && !k.active) return;  // EPI: idle waves still join the barriers
+    const uint32_t p = a.ep.parity;
+
+    V16 rv, wv;
+    if (EPI) {
+        rv = ld16(a.residual + k.row);
+        wv = ld16(a.weight + k.elem);
+    }
+    const uint32_t g = epoch_of(a.ep);
+    V16 v[N];
+    uint32_t attempts, first, last;
+    gather<N, MODE, false, true>(a, k, g, p, lane, v, attempts, first, last);
+    const V16 o = sum_round<N>(v);
+    if (k.active && lane == 0) {
+        write_log(a, k, g, log_word(attempts, first, last));
+        a.consumed[static_cast<size_t>(p) * geo.w_max + k.c] = g;
+    }
+    if (!EPI) {
+        if (k.lane_ok) st16(a.out + k.row, o);
+        return;
+    }
+    residual_rmsnorm(a, k, g, p, o, rv, wv, a.y, lane, wave, G, blockIdx.x);
+}
+
+// ---------------------------------------------------------------------------
+// Persistent decode step: one launch runs all L all-reduces. All waves are
+// co-resident (the host checks), and every wait is bounded.
+//
+// Per chunk and epoch g of parity p:
+//   producer  wait until consumed[p] == produced[p] (the reduction that read
+//             this slot two epochs back has finished: dual buffering), copy
+//             the N partials, agent-scope release fence, store the on-time
+//             stamps and produced[p] = g; injected late ranks' stamps follow
+//             after `late_delay` sleeps.
+//   consumer  stamps, then payload, through agent-scope loads (SPEC; ORDERED
+//             acquires the stamps first); retry with backoff while stale;
+//             sum; store; consumed[p] = g once every payload load has
+//             completed.
+// The producer can run one epoch ahead of the consumer, no further.
+// Producer wave of chunk (t, s), one epoch after the other: wait until the
+// slot of this parity is free, copy, one agent-scope release fence, stamps.
+// (Measured on MI355X: prefetching the next epoch's sources or batching
+// several chunks per wave behind one fence makes the step slower -- the
+// consumer then reaches each epoch before its stamps and pays a retry, and the
+// dual-buffer rule ties the producer of g + 1 to the reduction of g - 1.)
+template <int N, int MODE, bool EPI>
+__device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base, int lane) {
+    const ProduceArgs &a = A.p;
+    const Geometry &geo = a.geo;
+    const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x, lane);
+    for (int i = 0; i < A.reduces; ++i) {
+        const uint32_t g = base + static_cast<uint32_t>(i) + 1u;
+        const uint32_t p = static_cast<uint32_t>(i + 1) & 1u;
+        const size_t pc = static_cast<size_t>(p) * geo.w_max + k.c;
+        uint32_t spins = 0;
+        bool free = false;
+        while (true) {
+            free = ld_relaxed(a.consumed + pc) == ld_relaxed(a.produced + pc);
+            if (free || ++spins >= A.r.spin_limit || latched(a.err)) break;
+            __builtin_amdgcn_s_sleep(1);
+        }
+        if (!free) {
+            if (lane == 0) latch(a.err, kErrWaw, g, k.c, spins);
+            return;
+        }
+        copy_chunk<N>(a, k, g, p);
+        const uint32_t held = held_back(a.inject, a.inject_entries, g);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        uint32_t *stamp = a.stamps + pc * N;
+        if (lane < N && !((held >> lane) & 1u)) st_relaxed(stamp + lane, g);
+        if (lane == 0) st_relaxed(a.produced + pc, g);
+        if (held) {
+            const uint32_t inj = a.inject[(g - 1u) % static_cast<uint32_t>(a.inject_entries)];
+            for (uint32_t d = 0; d < A.late_delay; ++d) __builtin_amdgcn_s_sleep(8);
+            if (lane < N && ((inj >> lane) & 1u) && !((inj >> (8 + lane)) & 1u))
+                st_relaxed(stamp + lane, g);
+        }
+    }
+}
+
+template <int N, int MODE, bool EPI>
+__device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base, int lane) {
+    const ReduceArgs &a = A.r;
+    const Geometry &geo = a.geo;
+    const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x, lane);
+    V16 wv;
+    if (EPI) wv = ld16(a.weight + k.elem);
+    for (int i = 0; i < A.reduces; ++i) {
+        const uint32_t g = base + static_cast<uint32_t>(i) + 1u;
+        const uint32_t p = static_cast<uint32_t>(i + 1) & 1u;
+        V16 rv;
+        if (EPI) rv = ld16(a.residual + k.row);  // this wave's own previous store
+        V16 v[N];
+        uint32_t attempts, first, last;
+        gather<N, MODE, true, false>(a, k, g, p, lane, v, attempts, first, last);
+        const V16 o = sum_round<N>(v);
+        complete(o);  // every payload load has returned before the slot is released
+        if (lane == 0) {
+            write_log(a, k, g, log_word(attempts, first, last));
+            st_relaxed(a.consumed + static_cast<size_t>(p) * geo.w_max + k.c, g);
+        }
+        const uint64_t ring = static_cast<uint64_t>(i) * A.ring_stride;
+        if (!EPI) {
+            if (k.lane_ok) st16(a.out + ring + k.row, o);
+        } else {
+            residual_rmsnorm(a, k, g, p, o, rv, wv, a.y + ring, lane, 0, 1, blockIdx.x);
+        }
+        if (latched(a.err)) return;  // a bounded wait failed somewhere: stop the step
+    }
+}
+
+// Grid (segs, tokens, 2) of one-wave workgroups: plane 0 reduces chunk (t, s)
+// for epochs base+1 .. base+L in order, plane 1 produces it. The last wave to
+// arrive on the counter advances the epoch base for the next step: every wave
+// read the base before it arrived, so no wave can see the advanced value.
+template <int N, int MODE, bool EPI>
+__global__ __launch_bounds__(64) void chain_kernel(ChainArgs A) {
+    const int lane = threadIdx.x;
+    const uint32_t base = A.r.ep.base[0];
+    if (blockIdx.z == 1)
+        chain_producer<N, MODE, EPI>(A, base, lane);
+    else
+        chain_consumer<N, MODE, EPI>(A, base, lane);
+    if (lane == 0) {
+        const uint32_t waves = 2u * gridDim.x * gridDim.y;
+        const uint32_t before =
+            __hip_atomic_fetch_add(A.done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (before == waves - 1u) {
+            st_relaxed(A.done, 0u);
+            st_relaxed(A.epoch_base, base + A.advance);
+        }
+    }
 }
 
 __global__ void advance_kernel(uint32_t *base, uint32_t step) {
@@ -371,6 +576,78 @@ hipError_t launch_reduce_n(const ReduceArgs &a, const ProduceArgs *pa, int mode,
     return hipErrorInvalidValue;
 }
 
+template <int N, int MODE>
+const void *chain_fn(bool epi) {
+    return epi ? reinterpret_cast<const void *>(chain_kernel<N, MODE, true>)
+               : reinterpret_cast<const void *>(chain_kernel<N, MODE, false>);
+}
+
+template <int N>
+const void *chain_fn_n(int mode, bool epi) {
+    switch (mode) {
+        case kSpec: return chain_fn<N, kSpec>(epi);
+        case kOrdered: return chain_fn<N, kOrdered>(epi);
+        case kNone: return chain_fn<N, kNone>(epi);
+    }
+    return nullptr;
+}
+
+const void *chain_fn_any(int nranks, int mode, bool epi) {
+    switch (nranks) {
+        case 1: return chain_fn_n<1>(mode, epi);
+        case 2: return chain_fn_n<2>(mode, epi);
+        case 3: return chain_fn_n<3>(mode, epi);
+        case 4: return chain_fn_n<4>(mode, epi);
+        case 5: return chain_fn_n<5>(mode, epi);
+        case 6: return chain_fn_n<6>(mode, epi);
+        case 7: return chain_fn_n<7>(mode, epi);
+        case 8: return chain_fn_n<8>(mode, epi);
+    }
+    return nullptr;
+}
+
+template <int N, int MODE>
+const void *reduce_fn(bool epi) {
+    // the fused variant is the larger of the two: use it for occupancy
+    return epi ? reinterpret_cast<const void *>(reduce_kernel<N, MODE, true, true>)
+               : reinterpret_cast<const void *>(reduce_kernel<N, MODE, false, true>);
+}
+
+template <int N>
+const void *reduce_fn_n(int mode, bool epi) {
+    switch (mode) {
+        case kSpec: return reduce_fn<N, kSpec>(epi);
+        case kOrdered: return reduce_fn<N, kOrdered>(epi);
+        case kNone: return reduce_fn<N, kNone>(epi);
+    }
+    return nullptr;
+}
+
+const void *reduce_fn_any(int nranks, int mode, bool epi) {
+    switch (nranks) {
+        case 1: return reduce_fn_n<1>(mode, epi);
+        case 2: return reduce_fn_n<2>(mode, epi);
+        case 3: return reduce_fn_n<3>(mode, epi);
+        case 4: return reduce_fn_n<4>(mode, epi);
+        case 5: return reduce_fn_n<5>(mode, epi);
+        case 6: return reduce_fn_n<6>(mode, epi);
+        case 7: return reduce_fn_n<7>(mode, epi);
+        case 8: return reduce_fn_n<8>(mode, epi);
+    }
+    return nullptr;
+}
+
+int resident_groups(const void *fn, int threads) {
+    if (!fn) return 0;
+    int per_cu = 0, dev = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, 0) != hipSuccess)
+        return 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    return per_cu * cus;
+}
+
 }  // namespace
 
 hipError_t launch_produce(const ProduceArgs &a, int waves_per_group, hipStream_t s) {
@@ -411,32 +688,22 @@ hipError_t launch_reduce(const ReduceArgs &a, const ProduceArgs *next, int mode,
     return hipErrorInvalidValue;
 }
 
+hipError_t launch_chain(const ChainArgs &a, int mode, bool epilogue, hipStream_t s) {
+    const void *fn = chain_fn_any(a.r.geo.nranks, mode, epilogue);
+    if (!fn) return hipErrorInvalidValue;
+    if (a.r.geo.segs != a.p.geo.segs || a.r.geo.tokens != a.p.geo.tokens)
+        return hipErrorInvalidValue;
+    const dim3 grid(static_cast<uint32_t>(a.r.geo.segs), static_cast<uint32_t>(a.r.geo.tokens), 2);
+    void *args[] = {const_cast<ChainArgs *>(&a)};
+    return hipLaunchKernel(fn, grid, dim3(kLanes), args, 0, s);
+}
+
 int max_active_groups(int nranks, int mode, bool epilogue, int waves_per_group) {
-    const void *fn = nullptr;
-#define SIFAR_PICK(NN)                                                                  \
-    if (nranks == NN) {                                                                 \
-        if (mode == kSpec)                                                              \
-            fn = epilogue ? (const void *)reduce_kernel<NN, kSpec, true, true>          \
-                          : (const void *)reduce_kernel<NN, kSpec, false, false>;       \
-        else if (mode == kOrdered)                                                      \
-            fn = epilogue ? (const void *)reduce_kernel<NN, kOrdered, true, true>       \
-                          : (const void *)reduce_kernel<NN, kOrdered, false, false>;    \
-        else                                                                            \
-            fn = epilogue ? (const void *)reduce_kernel<NN, kNone, true, true>          \
-                          : (const void *)reduce_kernel<NN, kNone, false, false>;       \
-    }
-    SIFAR_PICK(1) SIFAR_PICK(2) SIFAR_PICK(3) SIFAR_PICK(4)
-    SIFAR_PICK(5) SIFAR_PICK(6) SIFAR_PICK(7) SIFAR_PICK(8)
-#undef SIFAR_PICK
-    if (!fn) return 0;
-    int per_cu = 0, dev = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, waves_per_group * kLanes, 0) !=
-        hipSuccess)
-        return 0;
-    if (hipGetDevice(&dev) != hipSuccess) return 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        return 0;
-    return per_cu * cus;
+    return resident_groups(reduce_fn_any(nranks, mode, epilogue), waves_per_group * kLanes);
+}
+
+int max_active_chain_groups(int nranks, int mode, bool epilogue) {
+    return resident_groups(chain_fn_any(nranks, mode, epilogue), kLanes);
 }
 
 hipError_t launch_advance(uint32_t *epoch_base, uint32_t step, hipStream_t s) {

@@ -18,6 +18,7 @@ struct DevState {
     uint32_t epoch_base;   // graph nodes compute g = epoch_base + node offset
     uint32_t zero;         // always 0: eager launches pass g as the offset
     uint32_t err[4];       // kind, epoch, chunk, attempts (first error wins)
+    uint32_t chain_done;   // waves of the running persistent step that have finished
 };
 
 // Geometry common to the producer and the reduction.
@@ -44,6 +45,7 @@ struct ProduceArgs {
     uint16_t *slots;             // [N][2][slot_elems]
     uint32_t *stamps;            // [2][w_max][N]
     const uint32_t *consumed;    // [2][w_max]: last epoch whose reduction finished the chunk
+    uint32_t *produced;          // [2][w_max]: last epoch written into the chunk's slots
     const uint16_t *src;         // entry e, rank r: src + e*entry_stride + r*rank_stride
     int64_t entry_stride;
     int64_t rank_stride;
@@ -70,10 +72,25 @@ struct ReduceArgs {
     uint16_t *residual;          // epilogue: [tokens][hidden], in place
     const uint16_t *weight;      // [hidden]
     uint16_t *y;                 // [tokens][hidden]
-    uint64_t *exch;              // [max_tokens][groups_per_token]: (epoch << 32) | partial bits
+    uint64_t *exch;              // [2][max_tokens][groups_per_token]: (epoch << 32) | partial bits
     int32_t groups_per_token;
+    int32_t exch_parity_stride;  // max_tokens * groups_per_token
     float eps;
     uint32_t *err;
+};
+
+// One launch running a whole decode step: consumer waves (plane 0) reduce the
+// L epochs one after another while producer waves (plane 1) play the peers,
+// concurrently, synchronised only through stamps and consumed/produced words.
+struct ChainArgs {
+    ReduceArgs r;                // r.out / r.y point at ring entry 0
+    ProduceArgs p;
+    int32_t reduces;             // L
+    uint64_t ring_stride;        // elements between ring entries
+    uint32_t late_delay;         // injected late stamps land after this many sleeps
+    uint32_t *epoch_base;        // advanced by `advance` by the last wave to finish
+    uint32_t advance;
+    uint32_t *done;              // arrival counter of the step's waves (left at 0)
 };
 
 enum Mode : int { kSpec = 0, kOrdered = 1, kNone = 2 };
@@ -85,6 +102,9 @@ hipError_t launch_reduce(const ReduceArgs &a, const ProduceArgs *next, int mode,
 // Workgroups of the reduction kernel that can be resident at once on the
 // current device (0 if unknown).
 int max_active_groups(int nranks, int mode, bool epilogue, int waves_per_group);
+// Same for the one-wave workgroups of the persistent chain kernel.
+int max_active_chain_groups(int nranks, int mode, bool epilogue);
+hipError_t launch_chain(const ChainArgs &a, int mode, bool epilogue, hipStream_t s);
 hipError_t launch_advance(uint32_t *epoch_base, uint32_t step, hipStream_t s);
 hipError_t launch_set_base(uint32_t *epoch_base, uint32_t value, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t *p, uint32_t value, uint64_t count, hipStream_t s);

@@ -324,3 +324,120 @@ def test_epilogue_residual_chain_every_node_eager():
             assert np.array_equal(to_host(res_d), res)
             assert ulp_distance(to_host(y), yy).max() <= 1
         s.check()
+
+
+# ---- persistent decode step: producers and reduction in one launch ----------
+
+@pytest.mark.parametrize("mode", ["spec", "ordered"])
+def test_persistent_llama_decode_steps(mode):
+    """One launch per decode step, the peers writing while the reduction runs:
+    every output bit-exact; every chunk's last validation clean."""
+    w = synth.LLAMA8B_DECODE
+    run = StepRun(w, 8, validate=mode, persistent=1)
+    for T in w.tokens:
+        for rep in range(3):
+            epochs = run.step(T)
+            run.s.check()
+            got = to_host(run.out_d)
+            exp = oracle.reduce_chain(run.pool, epochs, T)
+            for i in range(w.reduces_per_step):
+                assert np.array_equal(got[i, :T], exp[i]), f"T={T} rep={rep} node={i}"
+            log = run.s.read_log()[:, :T * 8]
+            assert np.all((log >> 24) == 0), "a chunk was accepted with a stale stamp"
+            assert np.all((log & 0xFFFF) >= 1)
+    run.s.close()
+
+
+def test_persistent_many_steps_sampled():
+    """100 persistent steps per batch size (the benchmark's shape), sampled."""
+    w = synth.LLAMA8B_DECODE
+    run = StepRun(w, 8, persistent=1)
+    for T in w.tokens:
+        for step in range(w.steps):
+            epochs = run.step(T)
+            if step % 11 == 0:
+                got = to_host(run.out_d)
+                for i in range(0, w.reduces_per_step, 5):
+                    g = epochs[i]
+                    exp = oracle.reduce(run.pool[(g - 1) % run.pool.shape[0]][:, :T])
+                    assert np.array_equal(got[i, :T], exp), f"T={T} step={step} node={i}"
+        run.s.check()
+    run.s.close()
+
+
+@pytest.mark.parametrize("order", ["spec", "ordered"])
+def test_persistent_late_stamps(order):
+    """Late ranks' stamps land after a delay while the reduction waits on them:
+    outputs equal the oracle; the decision log shows retries and ends clean."""
+    w = synth.SPEC_STRESS
+    steps = 6
+    late = synth.delay_table(w.wid, w.nranks, w.reduces_per_step * steps, w.stale_prob)
+    run = StepRun(w, 4, validate=order, persistent=1, late_delay=4)
+    run.s.set_injection(inject_table(late))
+    retried = 0
+    for step in range(steps):
+        epochs = run.step(4)
+        got = to_host(run.out_d)
+        exp = oracle.reduce_chain(run.pool, epochs, 4)
+        for i in range(w.reduces_per_step):
+            assert np.array_equal(got[i, :4], exp[i]), f"step={step} node={i}"
+        log = run.s.read_log()[:, :32]
+        assert np.all((log >> 24) == 0)
+        retried += int(np.count_nonzero((log & 0xFFFF) > 1))
+    run.s.check()
+    run.s.close()
+    assert retried > 0
+
+
+def test_persistent_withheld_stamp_latches():
+    w = synth.Workload(70, "withheld", 4, (2,), 1024, 8, 1, "normal")
+    run = StepRun(w, 2, persistent=1, max_attempts=64, spin_limit=1 << 14)
+    table = [0] * 16
+    table[4] = 0b0010 << 8      # epoch 5: rank 1's stamp never lands
+    run.s.set_injection(table)
+    run.step(2)
+    assert run.s.status() == S.SIFAR_EDEVICE
+    kind, epoch, chunk, attempts = run.s.error_info()
+    assert kind in (S.SIFAR_DEV_RETRY_BUDGET, S.SIFAR_DEV_WAW)
+    assert epoch >= 5
+    run.s.close()
+
+
+@pytest.mark.parametrize("T", [1, 8, 32])
+def test_persistent_epilogue_moe_chain(T):
+    """120 chained all-reduces + residual-add + RMSNorm in one launch per step."""
+    w = synth.MOE_DECODE
+    run = StepRun(w, 32, persistent=1)
+    res = run.res0[:T].copy()
+    for step in range(2):
+        epochs = run.step(T)
+        y_got = to_host(run.y_d)
+        _, r_list, y_list = oracle.reduce_chain(run.pool, epochs, T,
+                                                epilogue=(res, run.weight, w.rms_eps))
+        assert np.array_equal(to_host(run.res_d)[:T], r_list[-1])
+        for i in range(w.reduces_per_step):
+            assert ulp_distance(y_got[i, :T], y_list[i]).max() <= 1, f"step {step} node {i}"
+        res = r_list[-1]
+    run.s.check()
+    run.s.close()
+
+
+def test_persistent_after_eager_and_graph_steps():
+    """Eager epochs, fused graph steps and persistent steps on one handle."""
+    w = synth.Workload(71, "mixed-modes", 8, (2,), 4096, 6, 1, "act")
+    pool = synth.payload_pool(71, 8, 2, 4096, 19, "act")
+    run_p = StepRun(w, 2, persistent=1, pool=pool)
+    out = torch.zeros((2, 4096), dtype=torch.int16, device=DEV)
+    extra = to_dev(synth.payload_pool(72, 8, 2, 4096, 3, "act"))
+    extra_h = synth.payload_pool(72, 8, 2, 4096, 3, "act")
+    for k in range(3):
+        run_p.s.produce(extra[k], 2)
+        run_p.s.reduce(out, 2)
+        assert np.array_equal(to_host(out), oracle.reduce(extra_h[k]))
+        epochs = run_p.step(2)
+        got = to_host(run_p.out_d)
+        exp = oracle.reduce_chain(run_p.pool, epochs, 2)
+        for i in range(6):
+            assert np.array_equal(got[i, :2], exp[i]), (k, i)
+    run_p.s.check()
+    run_p.s.close()
