@@ -80,18 +80,22 @@ def graph_floor_us(nodes: int) -> float:
     return a.elapsed_time(b) * 1e3 / (reps * nodes)
 
 
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "fused_reduce_llama8b_decode_n8_h4096.md")
+TRAFFIC_PROFILES = {
+    "persistent": os.path.join(ROOT, "profiles", "chain_llama8b_decode_n8_h4096.md"),
+    "fused": os.path.join(ROOT, "profiles", "fused_reduce_llama8b_decode_n8_h4096.md"),
+}
 
 
-def measured_traffic():
-    """HBM bytes per launch of the fused kernel from the committed FETCH_SIZE /
+def measured_traffic(kind):
+    """HBM bytes per launch of the dominant kernel from the committed FETCH_SIZE /
     WRITE_SIZE profile, or None when the kernel source changed since."""
     import hashlib
 
-    if not os.path.exists(TRAFFIC_PROFILE):
+    path = TRAFFIC_PROFILES[kind]
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(TRAFFIC_PROFILE):
+    for line in open(path):
         if ":" in line and line.split(":")[0] in ("traffic_bytes_per_launch", "kernels_hip_sha256"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
@@ -391,8 +395,11 @@ def main():
     torch.cuda.synchronize()
     del calib, calib_dst
 
-    traffic = (measured_traffic() if (args.fuse and args.mode == "spec" and not args.persistent)
-               else None)
+    traffic = None
+    if args.mode == "spec" and args.persistent:
+        traffic = measured_traffic("persistent")
+    elif args.mode == "spec" and args.fuse:
+        traffic = measured_traffic("fused")
 
     cpu = None
     if args.cpu_seconds > 0:
