@@ -23,6 +23,7 @@ Printed JSON line (rank 0):
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -117,9 +118,12 @@ def parse():
     ap.add_argument("--persistent", type=int, default=1, choices=[0, 1],
                     help="1: one persistent launch per decode step (peers and reduction "
                          "concurrent); 0: one launch per all-reduce")
+    ap.add_argument("--buffers", type=int, default=2, choices=[1, 2],
+                    help="2: dual buffering; 1: one slot per rank (bottom barrier)")
     ap.add_argument("--floor-nodes", type=int, default=64)
     ap.add_argument("--workload", default="llama8b-decode",
-                    choices=["llama8b-decode", "smoke-n2", "spec-stress", "sweep", "moe-rmsnorm"],
+                    choices=["llama8b-decode", "smoke-n2", "spec-stress", "sweep", "moe-rmsnorm",
+                             "ablation", "retry-curve"],
                     help="llama8b-decode is the headline line; the others print one "
                          "JSON line per configuration")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -162,7 +166,7 @@ def time_steps(s, T, steps, stream):
 
 
 def chain_point(w, T, args, *, T_max=None, pool_entries=None, inject=False, waves_per_group=1,
-                check_nodes=(0, -1)):
+                check_nodes=(0, -1), forced=0):
     """Measure one captured chain configuration. Returns a JSON-ready dict."""
     import numpy as np
     import torch
@@ -181,7 +185,8 @@ def chain_point(w, T, args, *, T_max=None, pool_entries=None, inject=False, wave
         s = S.Sifar(nranks=N, hidden=H, max_tokens=T_max, reduces_per_step=L,
                     validate=args.mode, log_epochs=L, fuse_peers=args.fuse,
                     epilogue=int(w.epilogue), rms_eps=w.rms_eps,
-                    waves_per_group=waves_per_group, persistent=args.persistent)
+                    waves_per_group=waves_per_group, persistent=args.persistent,
+                    buffers=args.buffers, forced_retries=forced)
     except S.SifarError as err:
         if args.persistent and err.code == S.SIFAR_EINVAL:
             return {"workload": w.name, "nranks": N, "tokens": T, "hidden": H, "chain": L,
@@ -214,13 +219,14 @@ def chain_point(w, T, args, *, T_max=None, pool_entries=None, inject=False, wave
     epochs = list(range(nxt - L, nxt))
     out = {"workload": w.name, "nranks": N, "tokens": T, "hidden": H, "chain": L,
            "steps": args.steps, "us_per_reduce": ms * 1e3 / (args.steps * L)}
-    launches = 1 if args.persistent else (L + 2 if args.fuse else 2 * L + 1)
+    fused_launch = args.fuse and args.buffers == 2
+    launches = 1 if args.persistent else (L + 2 if fused_launch else 2 * L + 1)
     out["launch_period_us"] = ms * 1e3 / (args.steps * launches)
     K = T * H * 2
     red = reduce_bytes(N, T, H) + (3 * K + 2 * H if w.epilogue else 0)
     out["reduce_bytes"] = red
     out["reduce_gbs"] = red / (out["us_per_reduce"] * 1e-6) / 1e9
-    fused = red + (produce_bytes(N, T, H) if (args.fuse or args.persistent) else 0)
+    fused = red + (produce_bytes(N, T, H) if (fused_launch or args.persistent) else 0)
     if args.persistent:
         fused *= L
     out["launch_bytes"] = fused
@@ -244,7 +250,7 @@ def chain_point(w, T, args, *, T_max=None, pool_entries=None, inject=False, wave
         out["epochs_with_late_stamp_frac"] = float(np.mean([m != 0 for m in masks]))
         if not args.persistent:
             # launches in stream order: every decision is predictable exactly
-            pred = sim.predict_log(N, masks, args.mode)
+            pred = sim.predict_log(N, masks, args.mode, forced)
             assert all(np.all(rows[i] == pred[i]) for i in range(L)), "decision log != prediction"
             out["log_matches_prediction"] = True
     s.close()
@@ -262,6 +268,42 @@ def suite(args):
                chain_point(synth.SPEC_STRESS, 4, args, inject=False)]
     elif args.workload == "sweep":
         pts = [chain_point(w, w.tokens[0], args, pool_entries=5) for w in synth.PAYLOAD_SWEEP]
+    elif args.workload == "ablation":
+        # the paper's incremental optimisations (Sec. 6.3) as they exist here:
+        # one buffer (bottom barrier) -> dual buffering; ORDERED (top barrier by
+        # flag polling) -> SPEC (speculative); NONE = the "no barrier" ideal.
+        import copy
+        w = synth.LLAMA8B_DECODE
+        pts = []
+        combos = [(p_, b, m) for p_ in (0, 1) for b in (1, 2) for m in ("ordered", "spec", "none")
+                  if not (p_ and m == "none")]
+        for p_, b, m in combos:
+            a2 = copy.copy(args)
+            a2.persistent, a2.buffers, a2.mode = p_, b, m
+            for T in w.tokens:
+                pt = chain_point(w, T, a2, T_max=max(w.tokens))
+                pt.update(persistent=p_, buffers=b, validate=m)
+                pts.append(pt)
+        for p in pts:
+            print(json.dumps({k: (round(v, 4) if isinstance(v, float) else v)
+                              for k, v in p.items()}), flush=True)
+        return
+    elif args.workload == "retry-curve":
+        # forced retries (Sec. 6.3, "Retry Overhead") and late-stamp rates
+        import copy
+        w = synth.SPEC_STRESS
+        pts = []
+        for k in (0, 1, 2, 3, 4):
+            a2 = copy.copy(args)
+            a2.forced = k
+            pt = chain_point(w, 4, a2, forced=k)
+            pt.update(forced_retries=k)
+            pts.append(pt)
+        for prob in (0.0, 0.02, 0.05, 0.1, 0.2, 0.5):
+            wp = dataclasses.replace(w, stale_prob=prob)
+            pt = chain_point(wp, 4, args, inject=prob > 0)
+            pt.update(stale_prob=prob)
+            pts.append(pt)
     elif args.workload == "moe-rmsnorm":
         w = synth.MOE_DECODE
         pts = []
@@ -312,7 +354,8 @@ def main():
     pool_d = torch.from_numpy(pool.view(np.int16)).to(dev)
     ring = torch.zeros((L, T_max, H), dtype=torch.int16, device=dev)
     s = S.Sifar(nranks=N, hidden=H, max_tokens=T_max, reduces_per_step=L, validate=args.mode,
-                log_epochs=L, fuse_peers=args.fuse, persistent=args.persistent)
+                log_epochs=L, fuse_peers=args.fuse, persistent=args.persistent,
+                buffers=args.buffers)
     s.bind_step(pool_d, out_ring=ring)
     stream = torch.cuda.current_stream()
 
@@ -363,15 +406,16 @@ def main():
     # reduce(g_i)+produce(g_i+1) kernel, reduce(g_L) and the epoch advance:
     # the fused kernel is L-1 of the L+2 launches. Its average launch period
     # is the HIP-event step time over the launches of the step.
+    fused_launch = args.fuse and args.buffers == 2
     if args.persistent:
         launches, per_launch = 1, L
     else:
-        launches, per_launch = (L + 2 if args.fuse else 2 * L + 1), 1
+        launches, per_launch = (L + 2 if fused_launch else 2 * L + 1), 1
     kern = {}
     for T in tokens:
         period_us = per_t[T] * L / launches
         byts = per_launch * (reduce_bytes(N, T, H) +
-                             (produce_bytes(N, T, H) if (args.fuse or args.persistent) else 0))
+                             (produce_bytes(N, T, H) if (fused_launch or args.persistent) else 0))
         kern[T] = {"launch_period_us": period_us, "bytes_per_launch": byts,
                    "gbs": byts / (period_us * 1e-6) / 1e9}
     mean_period = sum(k["launch_period_us"] for k in kern.values()) / len(kern)
@@ -396,9 +440,9 @@ def main():
     del calib, calib_dst
 
     traffic = None
-    if args.mode == "spec" and args.persistent:
+    if args.mode == "spec" and args.buffers == 2 and args.persistent:
         traffic = measured_traffic("persistent")
-    elif args.mode == "spec" and args.fuse:
+    elif args.mode == "spec" and args.buffers == 2 and args.fuse:
         traffic = measured_traffic("fused")
 
     cpu = None
@@ -427,7 +471,7 @@ def main():
         "data": "synthetic (seeded N(0,1)*0.5 activations, 0.1% outliers x50)",
         "config": {"workload": w.name, "nranks": N, "hidden": H, "tokens": list(tokens),
                    "reduces_per_step": L, "validate": args.mode, "fuse_peers": args.fuse,
-                   "persistent": args.persistent,
+                   "persistent": args.persistent, "buffers": args.buffers,
                    "step": f"{len(tokens)} captured decode steps of {L} all-reduces"},
         "reduces_per_s": round(1e6 / us_per_reduce, 1),
         "us_per_reduce_by_tokens": {str(k): round(v, 4) for k, v in per_t.items()},

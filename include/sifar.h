@@ -83,7 +83,8 @@ typedef struct sifar_ctx *sifar_t;
  *          buffering" configuration of Sec. 3.4). Correct without any
  *          monotonicity assumption.
  * NONE     no stamps are read: the idealised "no barrier" configuration of
- *          Sec. 6.3. Only correct when stream order alone guarantees the data. */
+ *          Sec. 6.3. Only correct when stream order alone guarantees the data,
+ *          so not allowed with persistent steps. */
 #define SIFAR_VALIDATE_SPEC 0
 #define SIFAR_VALIDATE_ORDERED 1
 #define SIFAR_VALIDATE_NONE 2
@@ -122,11 +123,16 @@ typedef struct {
                                  needs 2 x max_tokens x ceil(hidden / 512) co-resident waves */
     uint32_t late_delay;      /* persistent steps with injection: a late rank's stamp lands
                                  this many ~0.2 us sleeps after its payload */
+    int32_t buffers;          /* 2: dual buffering (Sec. 3.3; no bottom barrier). 1: one slot per
+                                 rank, rewritten only after the previous all-reduce has finished
+                                 reading it -- the bottom barrier of Sec. 3.1, for the ablation
+                                 (no fused peers; the producer may not run ahead) */
 } sifar_config;
 
 /* Fills cfg with: N=8, H=4096, T_max=8, L=64, SPEC, no epilogue, eps=1e-6,
  * max_attempts=1<<20, forced_retries=0, spin_limit=1<<20, log_epochs=64,
- * waves_per_group=1, fuse_peers=1, persistent=0, late_delay=8. Never fails. */
+ * waves_per_group=1, fuse_peers=1, persistent=0, late_delay=8, buffers=2. Never
+ * fails. */
 void sifar_config_default(sifar_config *cfg);
 
 /* Library version: major * 10000 + minor * 100 + patch. */
@@ -145,7 +151,7 @@ void sifar_destroy(sifar_t h);
 /* ---- eager calls: one epoch at a time ---------------------------------------
  * Epochs are numbered from 1. The producer may run at most one epoch ahead of
  * the reduction: that is all two slots allow (Sec. 3.3); a third produce
- * before a reduce returns SIFAR_ESTATE. */
+ * before a reduce returns SIFAR_ESTATE (with buffers = 1, a second one). */
 
 /* The emulated peers write epoch g = next produced epoch. Rank r's partial is
  * read from src + r * src_rank_stride (elements), laid out [tokens][hidden]

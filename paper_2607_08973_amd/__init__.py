@@ -69,6 +69,7 @@ class sifar_config(ctypes.Structure):
         ("fuse_peers", ctypes.c_int32),
         ("persistent", ctypes.c_int32),
         ("late_delay", ctypes.c_uint32),
+        ("buffers", ctypes.c_int32),
     ]
 
 

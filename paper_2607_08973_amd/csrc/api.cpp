@@ -72,6 +72,9 @@ int check_cfg(const sifar_config *c) {
     if (g != 1 && g != 2 && g != 4 && g != 8 && g != 16) return SIFAR_EINVAL;
     if (c->fuse_peers != 0 && c->fuse_peers != 1) return SIFAR_EINVAL;
     if (c->persistent != 0 && c->persistent != 1) return SIFAR_EINVAL;
+    if (c->buffers != 1 && c->buffers != 2) return SIFAR_EINVAL;
+    // a live step without validation would read peers' slots mid-write
+    if (c->persistent && c->validate == SIFAR_VALIDATE_NONE) return SIFAR_EINVAL;
     return SIFAR_OK;
 }
 
@@ -143,6 +146,9 @@ ReduceArgs reduce_args(const sifar_t h, int32_t tokens, EpochRef ep) {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? SIFAR_OK : SIFAR_EHIP; }
 
+// Slot parity of epoch g is g & parity_mask: dual buffering, or one slot.
+uint32_t parity_mask(const sifar_t h) { return h->cfg.buffers == 2 ? 1u : 0u; }
+
 int launch_red(sifar_t h, const ReduceArgs &ra, const ProduceArgs *next, hipStream_t s) {
     return hip_status(launch_reduce(ra, next, h->cfg.validate, h->cfg.epilogue != 0,
                                     h->cfg.waves_per_group, s));
@@ -157,7 +163,7 @@ int capture_step(sifar_t h, int32_t tokens, hipGraphExec_t *out) {
     int rc = SIFAR_OK;
     auto node_args = [&](int i, ProduceArgs *pa, ReduceArgs *ra) {
         const EpochRef ep{&h->state->epoch_base, static_cast<uint32_t>(i + 1),
-                          static_cast<uint32_t>((i + 1) & 1)};
+                          static_cast<uint32_t>((i + 1) & 1) & parity_mask(h)};
         *pa = produce_args(h, tokens, ep, static_cast<const uint16_t *>(h->buf.src_pool),
                            h->buf.pool_entry_stride, h->buf.pool_rank_stride, h->buf.pool_entries);
         *ra = reduce_args(h, tokens, ep);
@@ -183,8 +189,9 @@ int capture_step(sifar_t h, int32_t tokens, hipGraphExec_t *out) {
         ca.epoch_base = &h->state->epoch_base;
         ca.advance = advance;
         ca.done = &h->state->chain_done;
+        ca.parity_mask = parity_mask(h);
         rc = hip_status(launch_chain(ca, h->cfg.validate, h->cfg.epilogue != 0, s));
-    } else if (h->cfg.fuse_peers) {
+    } else if (h->cfg.fuse_peers && h->cfg.buffers == 2) {
         node_args(0, &pa, &ra);
         rc = hip_status(launch_produce(pa, h->cfg.waves_per_group, s));
         for (int i = 0; i < L && rc == SIFAR_OK; ++i) {
@@ -235,6 +242,7 @@ void sifar_config_default(sifar_config *c) {
     c->fuse_peers = 1;
     c->persistent = 0;
     c->late_delay = 8;
+    c->buffers = 2;
 }
 
 int sifar_version(void) { return kVersion; }
@@ -352,9 +360,10 @@ int sifar_produce(sifar_t h, const void *src, int64_t src_rank_stride, int32_t t
     if (!src || !aligned16(src) || tokens < 1 || tokens > h->cfg.max_tokens) return SIFAR_EINVAL;
     if (src_rank_stride % 8 || src_rank_stride < static_cast<int64_t>(tokens) * h->cfg.hidden)
         return SIFAR_EINVAL;
-    if (h->next_prod - h->next_red > 1) return SIFAR_ESTATE;  // both slots hold unreduced epochs
+    // every slot holds an unreduced epoch
+    if (h->next_prod - h->next_red >= static_cast<uint32_t>(h->cfg.buffers)) return SIFAR_ESTATE;
     const uint32_t g = h->next_prod;
-    const EpochRef ep{&h->state->zero, g, g & 1u};
+    const EpochRef ep{&h->state->zero, g, g & parity_mask(h)};
     ProduceArgs pa = produce_args(h, tokens, ep, static_cast<const uint16_t *>(src), 0,
                                   src_rank_stride, 1);
     rc = hip_status(launch_produce(pa, h->cfg.waves_per_group, static_cast<hipStream_t>(stream)));
@@ -369,7 +378,7 @@ static int reduce_common(sifar_t h, int32_t tokens, void *stream, uint16_t *out,
     const uint32_t g = h->next_red;
     if (g >= h->next_prod) return SIFAR_ESTATE;  // nothing produced to reduce
     if (tokens != h->prod_tokens[g & 1u]) return SIFAR_EINVAL;
-    const EpochRef ep{&h->state->zero, g, g & 1u};
+    const EpochRef ep{&h->state->zero, g, g & parity_mask(h)};
     ReduceArgs ra = reduce_args(h, tokens, ep);
     ra.out = out;
     ra.residual = residual;

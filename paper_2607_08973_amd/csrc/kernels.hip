@@ -307,9 +307,9 @@ __device__ __forceinline__ void write_log(const ReduceArgs &a, const Chunk &k, u
 // Residual-add + RMSNorm of one chunk after its all-reduce result o. The
 // token's sum of squares is combined across the waves of the workgroup (LDS)
 // and across the token's Q workgroups (epoch-tagged exchange words, double
-// buffered by parity). Every wave of the workgroup must call this.
+// buffered by the epoch's parity). Every wave of the workgroup must call this.
 __device__ __forceinline__ void residual_rmsnorm(const ReduceArgs &a, const Chunk &k, uint32_t g,
-                                                 uint32_t p, const V16 &o, const V16 &rv,
+                                                 const V16 &o, const V16 &rv,
                                                  const V16 &wv, uint16_t *y, int lane, int wave,
                                                  int G, int q) {
     const Geometry &geo = a.geo;
@@ -344,7 +344,7 @@ __device__ __forceinline__ void residual_rmsnorm(const ReduceArgs &a, const Chun
     const int Q = a.groups_per_token;
     if (Q > 1) {
         if (wave == 0) {
-            uint64_t *ex = a.exch + static_cast<size_t>(p) * a.exch_parity_stride +
+            uint64_t *ex = a.exch + static_cast<size_t>(g & 1u) * a.exch_parity_stride +
                            static_cast<size_t>(k.t) * Q;
             if (lane == 0) {
                 const uint64_t word = (static_cast<uint64_t>(g) << 32) | __float_as_uint(grp);
@@ -419,7 +419,7 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
         if (k.lane_ok) st16(a.out + k.row, o);
         return;
     }
-    residual_rmsnorm(a, k, g, p, o, rv, wv, a.y, lane, wave, G, blockIdx.x);
+    residual_rmsnorm(a, k, g, o, rv, wv, a.y, lane, wave, G, blockIdx.x);
 }
 
 // ---------------------------------------------------------------------------
@@ -438,7 +438,9 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
 //             completed.
 // The producer can run one epoch ahead of the consumer, no further.
 // Producer wave of chunk (t, s), one epoch after the other: wait until the
-// slot of this parity is free, copy, one agent-scope release fence, stamps.
+// slot of this parity is free (with a single buffer: until the previous
+// epoch's reduction is done -- the bottom barrier), copy, one agent-scope
+// release fence, stamps.
 // (Measured on MI355X: prefetching the next epoch's sources or batching
 // several chunks per wave behind one fence makes the step slower -- the
 // consumer then reaches each epoch before its stamps and pays a retry, and the
@@ -450,7 +452,7 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
     const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x, lane);
     for (int i = 0; i < A.reduces; ++i) {
         const uint32_t g = base + static_cast<uint32_t>(i) + 1u;
-        const uint32_t p = static_cast<uint32_t>(i + 1) & 1u;
+        const uint32_t p = static_cast<uint32_t>(i + 1) & A.parity_mask;
         const size_t pc = static_cast<size_t>(p) * geo.w_max + k.c;
         uint32_t spins = 0;
         bool free = false;
@@ -487,7 +489,7 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
     if (EPI) wv = ld16(a.weight + k.elem);
     for (int i = 0; i < A.reduces; ++i) {
         const uint32_t g = base + static_cast<uint32_t>(i) + 1u;
-        const uint32_t p = static_cast<uint32_t>(i + 1) & 1u;
+        const uint32_t p = static_cast<uint32_t>(i + 1) & A.parity_mask;
         V16 rv;
         if (EPI) rv = ld16(a.residual + k.row);  // this wave's own previous store
         V16 v[N];
@@ -503,7 +505,7 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
         if (!EPI) {
             if (k.lane_ok) st16(a.out + ring + k.row, o);
         } else {
-            residual_rmsnorm(a, k, g, p, o, rv, wv, a.y + ring, lane, 0, 1, blockIdx.x);
+            residual_rmsnorm(a, k, g, o, rv, wv, a.y + ring, lane, 0, 1, blockIdx.x);
         }
         if (latched(a.err)) return;  // a bounded wait failed somewhere: stop the step
     }

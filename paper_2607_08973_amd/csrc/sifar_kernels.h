@@ -31,8 +31,9 @@ struct Geometry {
     uint64_t slot_elems;   // elements between consecutive slots
 };
 
-// Where the epoch of a launch comes from: g = *base + off. Parity is frozen at
-// launch (graph capture) time; the host guarantees *base is even for graphs.
+// Where the epoch of a launch comes from: g = *base + off. The slot parity is
+// frozen at launch (graph capture) time -- g & 1 with dual buffering (the host
+// keeps *base even for graphs), 0 with a single buffer.
 struct EpochRef {
     const uint32_t *base;
     uint32_t off;
@@ -91,6 +92,7 @@ struct ChainArgs {
     uint32_t *epoch_base;        // advanced by `advance` by the last wave to finish
     uint32_t advance;
     uint32_t *done;              // arrival counter of the step's waves (left at 0)
+    uint32_t parity_mask;        // 1: dual buffering (parity = epoch & 1); 0: one slot
 };
 
 enum Mode : int { kSpec = 0, kOrdered = 1, kNone = 2 };

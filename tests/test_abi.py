@@ -32,8 +32,8 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_struct_layouts_match_header():
-    # sifar_config: 15 four-byte fields; sifar_step_buffers: pointer/int64 layout
-    assert ctypes.sizeof(S.sifar_config) == 60
+    # sifar_config: 16 four-byte fields; sifar_step_buffers: pointer/int64 layout
+    assert ctypes.sizeof(S.sifar_config) == 64
     assert ctypes.sizeof(S.sifar_step_buffers) == 64
     text = open(HEADER).read()
     cfg = re.search(r"typedef struct \{([^{}]*)\} sifar_config;", text).group(1)
@@ -50,7 +50,7 @@ def test_defaults_and_strings():
     assert c.validate == S.SIFAR_VALIDATE_SPEC and c.epilogue == 0
     assert abs(c.rms_eps - 1e-6) < 1e-12
     assert c.max_attempts == 1 << 20 and c.waves_per_group == 1 and c.fuse_peers == 1
-    assert c.persistent == 0 and c.late_delay == 8
+    assert c.persistent == 0 and c.late_delay == 8 and c.buffers == 2
     assert S.sifar_version() >= 100
     for code in (0, -1, -2, -3, -4, -5):
         assert S.strerror(code)
@@ -61,7 +61,7 @@ def test_defaults_and_strings():
     ("nranks", 0), ("nranks", 9), ("hidden", 4), ("hidden", 4100), ("hidden", 65544),
     ("max_tokens", 0), ("reduces_per_step", 0), ("validate", 3), ("epilogue", 2),
     ("max_attempts", 0), ("spin_limit", 0), ("log_epochs", 0), ("waves_per_group", 3),
-    ("waves_per_group", 32), ("fuse_peers", 2), ("persistent", 2),
+    ("waves_per_group", 32), ("fuse_peers", 2), ("persistent", 2), ("buffers", 0), ("buffers", 3),
 ])
 def test_invalid_config_rejected_on_host(field, value):
     c = S.sifar_config_default()
@@ -69,6 +69,14 @@ def test_invalid_config_rejected_on_host(field, value):
     h = ctypes.c_void_p()
     rc = S.load().sifar_init(ctypes.byref(c), ctypes.byref(h))
     assert rc == S.SIFAR_EINVAL and not h.value
+
+
+def test_persistent_without_validation_rejected():
+    c = S.sifar_config_default()
+    c.persistent = 1
+    c.validate = S.SIFAR_VALIDATE_NONE
+    h = ctypes.c_void_p()
+    assert S.load().sifar_init(ctypes.byref(c), ctypes.byref(h)) == S.SIFAR_EINVAL
 
 
 def test_null_handle_rejected():

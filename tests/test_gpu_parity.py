@@ -441,3 +441,56 @@ def test_persistent_after_eager_and_graph_steps():
             assert np.array_equal(got[i, :2], exp[i]), (k, i)
     run_p.s.check()
     run_p.s.close()
+
+
+# ---- one buffer per rank: the bottom-barrier baseline ----------------------
+
+@pytest.mark.parametrize("persistent", [0, 1])
+@pytest.mark.parametrize("mode", ["spec", "ordered"])
+def test_single_buffer_steps(mode, persistent):
+    """buffers = 1: each rank has one slot, rewritten only after the previous
+    all-reduce finished reading it. Same outputs, bit-exact."""
+    w = synth.LLAMA8B_DECODE
+    run = StepRun(w, 8, validate=mode, persistent=persistent, buffers=1)
+    for T in (1, 8):
+        for rep in range(2):
+            epochs = run.step(T)
+            got = to_host(run.out_d)
+            exp = oracle.reduce_chain(run.pool, epochs, T)
+            for i in range(w.reduces_per_step):
+                assert np.array_equal(got[i, :T], exp[i]), f"T={T} rep={rep} node={i}"
+    run.s.check()
+    run.s.close()
+
+
+def test_single_buffer_eager_order():
+    N, T, H = 4, 1, 1024
+    pool = synth.payload_pool(9, N, T, H, 3, "normal")
+    src = to_dev(pool)
+    out = torch.zeros((T, H), dtype=torch.int16, device=DEV)
+    with S.Sifar(nranks=N, hidden=H, max_tokens=T, reduces_per_step=2, buffers=1) as s:
+        s.produce(src[0], T)
+        with pytest.raises(S.SifarError) as e:
+            s.produce(src[1], T)   # the only slot still holds epoch 1
+        assert e.value.code == S.SIFAR_ESTATE
+        s.reduce(out, T)
+        assert np.array_equal(to_host(out), oracle.reduce(pool[0]))
+        s.produce(src[1], T)
+        s.reduce(out, T)
+        assert np.array_equal(to_host(out), oracle.reduce(pool[1]))
+        s.check()
+
+
+def test_single_buffer_epilogue_persistent():
+    w = synth.MOE_DECODE
+    run = StepRun(w, 8, persistent=1, buffers=1)
+    T = 8
+    res = run.res0[:T].copy()
+    epochs = run.step(T)
+    y_got = to_host(run.y_d)
+    _, r_list, y_list = oracle.reduce_chain(run.pool, epochs, T, epilogue=(res, run.weight, w.rms_eps))
+    assert np.array_equal(to_host(run.res_d)[:T], r_list[-1])
+    for i in range(w.reduces_per_step):
+        assert ulp_distance(y_got[i, :T], y_list[i]).max() <= 1
+    run.s.check()
+    run.s.close()
