@@ -52,6 +52,34 @@ def produce_bytes(N: int, T: int, H: int) -> int:
     return 2 * N * K + 4 * N * chunks
 
 
+def latency_floors() -> dict:
+    """The library's latency probes (sifar_floor): launch and graph-node
+    floors, one agent-scope atomic, acquire / coherent / L2 / cache-missing
+    load, a release fence after a store, and a release -> acquire handoff
+    across and within an XCD."""
+    import paper_2607_08973_amd as S
+
+    probes = (  # (name in the JSON line, kind, operations, scale from ns)
+        ("graph_node_us", S.SIFAR_FLOOR_GRAPH_NODE, 256, 1e-3),
+        ("eager_launch_us", S.SIFAR_FLOOR_EAGER_LAUNCH, 256, 1e-3),
+        ("atomic_ns", S.SIFAR_FLOOR_ATOMIC, 4096, 1.0),
+        ("acquire_load_ns", S.SIFAR_FLOOR_ACQUIRE_LOAD, 4096, 1.0),
+        ("coherent_load_ns", S.SIFAR_FLOOR_COHERENT_LOAD, 4096, 1.0),
+        ("l2_load_ns", S.SIFAR_FLOOR_L2_LOAD, 4096, 1.0),
+        ("cold_load_ns", S.SIFAR_FLOOR_COLD_LOAD, 2048, 1.0),
+        ("release_fence_ns", S.SIFAR_FLOOR_RELEASE_FENCE, 4096, 1.0),
+        ("handoff_cross_xcd_ns", S.SIFAR_FLOOR_PINGPONG_XCD, 4096, 1.0),
+        ("handoff_same_xcd_ns", S.SIFAR_FLOOR_PINGPONG_SAME_XCD, 4096, 1.0),
+    )
+    out = {}
+    for name, kind, ops, scale in probes:
+        ns, info = S.sifar_floor(kind, ops)
+        out[name] = round(ns * scale, 4 if scale != 1.0 else 1)
+        if kind in (S.SIFAR_FLOOR_PINGPONG_XCD, S.SIFAR_FLOOR_PINGPONG_SAME_XCD):
+            out[name.replace("_ns", "_xccs")] = info[1:3]
+    return out
+
+
 def graph_floor_us(nodes: int) -> float:
     """Per-node time of a captured graph of minimal kernels (one-element
     in-place add): the dispatch floor every launch of a chain pays."""
@@ -400,6 +428,7 @@ def main():
 
     # ---- dispatch floor: a captured graph of tiny kernels ------------------
     floor_us = graph_floor_us(args.floor_nodes)
+    floors = latency_floors()
 
     # ---- roofline of the dominant kernel -----------------------------------
     # With fused peers a step is produce(g1), L-1 launches of the fused
@@ -478,6 +507,7 @@ def main():
         "dominant_kernel": {str(k): {kk: (round(vv, 4) if isinstance(vv, float) else vv)
                                      for kk, vv in v.items()} for k, v in kern.items()},
         "graph_dispatch_floor_us": round(floor_us, 4),
+        "floors": floors,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
                      "traffic": traffic, "bytes_per_launch": round(mean_bytes),

@@ -251,6 +251,54 @@ int sifar_error_info(sifar_t h, uint32_t info[4]);
 /* Static string for a return code. */
 const char *sifar_strerror(int code);
 
+/* ---- Latency floors --------------------------------------------------------
+ * The yardsticks a small all-reduce is read against (the paper times its
+ * all-reduces back to back inside one persistent kernel to leave launch
+ * overhead out, Sec. 6.1; on one GPU the launch gap and the cost of one
+ * coherent memory round trip are what a small all-reduce is made of).
+ * Needs no handle. Each kind measures `iterations` operations and writes the
+ * mean nanoseconds per operation to *ns_per_op:
+ *
+ *  GRAPH_NODE        a captured hipGraph of `iterations` empty one-wave
+ *                    kernels, replayed; ns per node (iterations <= 4096)
+ *  EAGER_LAUNCH      `iterations` eager launches of the same kernel; ns each
+ *                    (iterations <= 4096)
+ *  ATOMIC            dependent agent-scope fetch-and-add on one word
+ *  ACQUIRE_LOAD      dependent agent-scope acquire loads of one word (a load
+ *                    plus the L2 invalidate that acquire implies)
+ *  COHERENT_LOAD     dependent agent-scope relaxed loads of one word
+ *  L2_LOAD           dependent loads walking a 1 MiB ring line by line
+ *                    (L2 hits: the ring does not fit the L1)
+ *  COLD_LOAD         dependent loads over a 1 GiB ring, each in a new line
+ *                    and a new 4 MiB region, after the ring was pushed out of
+ *                    L2 and the Infinity Cache (misses every cache and the
+ *                    translation caches; iterations <= 65536)
+ *  RELEASE_FENCE     a 16-byte store followed by an agent-scope release fence
+ *  PINGPONG_XCD      one-way release -> acquire handoff between two waves on
+ *                    different XCDs (iterations round trips, <= 65536)
+ *  PINGPONG_SAME_XCD the same between two waves on one XCD
+ *
+ * info[0] is 1 when the probe completed, info[1] and info[2] the XCD (XCC_ID)
+ * the probe's first and second wave ran on (0 for host-timed kinds).
+ * Synchronises `stream`; allocates and frees its own device memory (1.5 GiB
+ * for COLD_LOAD). Returns SIFAR_EINVAL for an unknown kind, a null pointer or
+ * iterations out of range, SIFAR_ENOMEM, SIFAR_EHIP, or SIFAR_EDEVICE when a
+ * handoff's bounded wait gave up (the partner wave never answered). */
+enum {
+    SIFAR_FLOOR_GRAPH_NODE = 0,
+    SIFAR_FLOOR_EAGER_LAUNCH = 1,
+    SIFAR_FLOOR_ATOMIC = 2,
+    SIFAR_FLOOR_ACQUIRE_LOAD = 3,
+    SIFAR_FLOOR_COHERENT_LOAD = 4,
+    SIFAR_FLOOR_L2_LOAD = 5,
+    SIFAR_FLOOR_COLD_LOAD = 6,
+    SIFAR_FLOOR_RELEASE_FENCE = 7,
+    SIFAR_FLOOR_PINGPONG_XCD = 8,
+    SIFAR_FLOOR_PINGPONG_SAME_XCD = 9
+};
+int sifar_floor(int32_t kind, int32_t iterations, void *stream, double *ns_per_op,
+                uint32_t info[4]);
+
 #ifdef __cplusplus
 }
 #endif

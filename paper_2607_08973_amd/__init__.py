@@ -41,6 +41,18 @@ VALIDATE = {"spec": 0, "ordered": 1, "none": 2}
 SIFAR_INJECT_OFF = 0
 SIFAR_INJECT_DETERMINISTIC = 1
 
+# latency floors (sifar_floor kinds)
+SIFAR_FLOOR_GRAPH_NODE = 0
+SIFAR_FLOOR_EAGER_LAUNCH = 1
+SIFAR_FLOOR_ATOMIC = 2
+SIFAR_FLOOR_ACQUIRE_LOAD = 3
+SIFAR_FLOOR_COHERENT_LOAD = 4
+SIFAR_FLOOR_L2_LOAD = 5
+SIFAR_FLOOR_COLD_LOAD = 6
+SIFAR_FLOOR_RELEASE_FENCE = 7
+SIFAR_FLOOR_PINGPONG_XCD = 8
+SIFAR_FLOOR_PINGPONG_SAME_XCD = 9
+
 CHUNK = 512  # elements per chunk (one 64-lane wave, 16 bytes per lane)
 
 # every symbol include/sifar.h declares
@@ -48,7 +60,7 @@ EXPORTS = (
     "sifar_config_default", "sifar_version", "sifar_init", "sifar_destroy",
     "sifar_produce", "sifar_reduce", "sifar_reduce_rmsnorm", "sifar_bind_step",
     "sifar_step", "sifar_set_injection", "sifar_log_geometry", "sifar_read_log",
-    "sifar_epochs", "sifar_status", "sifar_error_info", "sifar_strerror",
+    "sifar_epochs", "sifar_status", "sifar_error_info", "sifar_strerror", "sifar_floor",
 )
 
 
@@ -130,6 +142,8 @@ def load(path: str = LIB_PATH):
         "sifar_status": (ctypes.c_int, [P]),
         "sifar_error_info": (ctypes.c_int, [P, ctypes.POINTER(U32)]),
         "sifar_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+        "sifar_floor": (ctypes.c_int, [I32, I32, P, ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(U32)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -246,6 +260,15 @@ def sifar_error_info(h: int):
     info = (ctypes.c_uint32 * 4)()
     _check("sifar_error_info", load().sifar_error_info(h, info))
     return list(info)
+
+
+def sifar_floor(kind: int, iterations: int, stream=None):
+    """One latency floor: returns (ns per operation, [completed, xcc_a, xcc_b, 0])."""
+    ns = ctypes.c_double()
+    info = (ctypes.c_uint32 * 4)()
+    _check("sifar_floor", load().sifar_floor(kind, iterations, _stream(stream),
+                                             ctypes.byref(ns), info))
+    return ns.value, list(info)
 
 
 def sifar_status(h: int) -> int:

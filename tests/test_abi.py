@@ -86,3 +86,28 @@ def test_null_handle_rejected():
     assert L.sifar_status(None) == S.SIFAR_EINVAL
     assert L.sifar_init(None, None) == S.SIFAR_EINVAL
     L.sifar_destroy(None)
+
+
+def test_floor_constants_match_header():
+    text = open(HEADER).read()
+    block = re.search(r"enum \{([^{}]*SIFAR_FLOOR_[^{}]*)\};", text).group(1)
+    pairs = dict((k, int(v)) for k, v in re.findall(r"(SIFAR_FLOOR_\w+)\s*=\s*(\d+)", block))
+    assert len(pairs) == 10
+    for k, v in pairs.items():
+        assert getattr(S, k) == v, k
+
+
+@pytest.mark.parametrize("kind,iterations", [
+    (-1, 10), (10, 10),                                   # unknown kinds
+    (S.SIFAR_FLOOR_ATOMIC, 0), (S.SIFAR_FLOOR_ATOMIC, (1 << 20) + 1),
+    (S.SIFAR_FLOOR_GRAPH_NODE, 4097), (S.SIFAR_FLOOR_EAGER_LAUNCH, 4097),
+    (S.SIFAR_FLOOR_COLD_LOAD, 65537), (S.SIFAR_FLOOR_PINGPONG_XCD, 65537),
+    (S.SIFAR_FLOOR_PINGPONG_SAME_XCD, 65537),
+])
+def test_floor_rejects_bad_arguments_on_host(kind, iterations):
+    L = S.load()
+    ns = ctypes.c_double(-1.0)
+    info = (ctypes.c_uint32 * 4)()
+    assert L.sifar_floor(kind, iterations, None, ctypes.byref(ns), info) == S.SIFAR_EINVAL
+    assert L.sifar_floor(S.SIFAR_FLOOR_ATOMIC, 10, None, None, info) == S.SIFAR_EINVAL
+    assert L.sifar_floor(S.SIFAR_FLOOR_ATOMIC, 10, None, ctypes.byref(ns), None) == S.SIFAR_EINVAL
