@@ -480,11 +480,71 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
     }
 }
 
-template <int N, int MODE, bool EPI>
-__device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base, int lane) {
+// Grouped producer (G waves per workgroup, one chunk per wave): the waves
+// copy their chunks, meet at a workgroup barrier, and wave 0 issues ONE
+// agent-scope release fence for all of them and stores every chunk's stamps
+// (lane = chunk wave * N + rank). An agent-scope release writes back the XCD's
+// L2 and fences of one XCD serialise, so sharing one fence among G chunks
+// shortens the epoch once several producer waves share each XCD. Every wave
+// reaches the barrier in every epoch; a failed slot wait ends the whole
+// workgroup at the same barrier.
+template <int N>
+__device__ __forceinline__ void chain_producer_grouped(const ChainArgs &A, uint32_t base,
+                                                       int lane, int wave, int G) {
+    const ProduceArgs &a = A.p;
+    const Geometry &geo = a.geo;
+    const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x * G + wave, lane);
+    const int sw = lane / N, sr = lane - sw * N;
+    const Chunk ks = chunk_at(geo, blockIdx.y, blockIdx.x * G + (sw < G ? sw : 0), 0);
+    const bool stamper = wave == 0 && sw < G && ks.active;
+    for (int i = 0; i < A.reduces; ++i) {
+        const uint32_t g = base + static_cast<uint32_t>(i) + 1u;
+        const uint32_t p = static_cast<uint32_t>(i + 1) & A.parity_mask;
+        bool free = true;
+        if (k.active) {
+            const size_t pc = static_cast<size_t>(p) * geo.w_max + k.c;
+            uint32_t spins = 0;
+            while (true) {
+                free = ld_relaxed(a.consumed + pc) == ld_relaxed(a.produced + pc);
+                if (free || ++spins >= A.r.spin_limit || latched(a.err)) break;
+                __builtin_amdgcn_s_sleep(1);
+            }
+            if (!free && lane == 0) latch(a.err, kErrWaw, g, k.c, spins);
+            if (free) {
+                copy_chunk<N>(a, k, g, p);
+                // only this wave reads its chunk's produced word: recording it
+                // here, not after wave 0's fence, keeps the next epoch's slot
+                // check from seeing the previous value (with one buffer that
+                // would let the slot be rewritten before it is consumed)
+                if (lane == 0) st_relaxed(a.produced + pc, g);
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's slot stores have reached L2
+        if (__syncthreads_or(!free)) return;
+        if (wave == 0) {
+            const uint32_t held = held_back(a.inject, a.inject_entries, g);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            const size_t ps = static_cast<size_t>(p) * geo.w_max + ks.c;
+            uint32_t *stamp = a.stamps + ps * N;
+            if (stamper && !((held >> sr) & 1u)) st_relaxed(stamp + sr, g);
+            if (held) {
+                const uint32_t inj = a.inject[(g - 1u) % static_cast<uint32_t>(a.inject_entries)];
+                for (uint32_t d = 0; d < A.late_delay; ++d) __builtin_amdgcn_s_sleep(8);
+                if (stamper && ((inj >> sr) & 1u) && !((inj >> (8 + sr)) & 1u))
+                    st_relaxed(stamp + sr, g);
+            }
+        }
+    }
+}
+
+// Consumer wave of chunk (t, x * G + wave). With G > 1 and the epilogue the
+// group's waves share the RMSNorm barriers, so they also leave together.
+template <int N, int MODE, bool EPI, bool GROUPED>
+__device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base, int lane,
+                                               int wave, int G) {
     const ReduceArgs &a = A.r;
     const Geometry &geo = a.geo;
-    const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x, lane);
+    const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x * G + wave, lane);
     V16 wv;
     if (EPI) wv = ld16(a.weight + k.elem);
     for (int i = 0; i < A.reduces; ++i) {
@@ -505,26 +565,39 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
         if (!EPI) {
             if (k.lane_ok) st16(a.out + ring + k.row, o);
         } else {
-            residual_rmsnorm(a, k, g, o, rv, wv, a.y + ring, lane, 0, 1, blockIdx.x);
+            residual_rmsnorm(a, k, g, o, rv, wv, a.y + ring, lane, wave, G, blockIdx.x);
         }
-        if (latched(a.err)) return;  // a bounded wait failed somewhere: stop the step
+        // a bounded wait failed somewhere: stop the step
+        if (GROUPED && EPI) {
+            if (__syncthreads_or(latched(a.err))) return;
+        } else if (latched(a.err)) {
+            return;
+        }
     }
 }
 
-// Grid (segs, tokens, 2) of one-wave workgroups: plane 0 reduces chunk (t, s)
-// for epochs base+1 .. base+L in order, plane 1 produces it. The last wave to
-// arrive on the counter advances the epoch base for the next step: every wave
-// read the base before it arrived, so no wave can see the advanced value.
-template <int N, int MODE, bool EPI>
-__global__ __launch_bounds__(64) void chain_kernel(ChainArgs A) {
-    const int lane = threadIdx.x;
+// Grid (segs / G, tokens, 2) of G-wave workgroups (G = 1, or kChainGroupWaves
+// when GROUPED): plane 0 reduces chunk (t, x * G + wave) for epochs
+// base+1 .. base+L in order, plane 1 produces it. The last wave to arrive on
+// the counter advances the epoch base for the next step: every wave read the
+// base before it arrived, so no wave can see the advanced value.
+template <int N, int MODE, bool EPI, bool GROUPED>
+__global__ __launch_bounds__(GROUPED ? kChainGroupWaves * kLanes : kLanes) void chain_kernel(
+    ChainArgs A) {
+    const int lane = threadIdx.x & (kLanes - 1);
+    const int wave = GROUPED ? static_cast<int>(threadIdx.x) / kLanes : 0;
+    const int G = GROUPED ? static_cast<int>(blockDim.x) / kLanes : 1;
     const uint32_t base = A.r.ep.base[0];
-    if (blockIdx.z == 1)
-        chain_producer<N, MODE, EPI>(A, base, lane);
-    else
-        chain_consumer<N, MODE, EPI>(A, base, lane);
+    if (blockIdx.z == 1) {
+        if (GROUPED)
+            chain_producer_grouped<N>(A, base, lane, wave, G);
+        else
+            chain_producer<N, MODE, EPI>(A, base, lane);
+    } else {
+        chain_consumer<N, MODE, EPI, GROUPED>(A, base, lane, wave, G);
+    }
     if (lane == 0) {
-        const uint32_t waves = 2u * gridDim.x * gridDim.y;
+        const uint32_t waves = 2u * gridDim.x * gridDim.y * static_cast<uint32_t>(G);
         const uint32_t before =
             __hip_atomic_fetch_add(A.done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (before == waves - 1u) {
@@ -579,31 +652,34 @@ hipError_t launch_reduce_n(const ReduceArgs &a, const ProduceArgs *pa, int mode,
 }
 
 template <int N, int MODE>
-const void *chain_fn(bool epi) {
-    return epi ? reinterpret_cast<const void *>(chain_kernel<N, MODE, true>)
-               : reinterpret_cast<const void *>(chain_kernel<N, MODE, false>);
+const void *chain_fn(bool epi, bool grouped) {
+    if (grouped)
+        return epi ? reinterpret_cast<const void *>(chain_kernel<N, MODE, true, true>)
+                   : reinterpret_cast<const void *>(chain_kernel<N, MODE, false, true>);
+    return epi ? reinterpret_cast<const void *>(chain_kernel<N, MODE, true, false>)
+               : reinterpret_cast<const void *>(chain_kernel<N, MODE, false, false>);
 }
 
 template <int N>
-const void *chain_fn_n(int mode, bool epi) {
+const void *chain_fn_n(int mode, bool epi, bool grouped) {
     switch (mode) {
-        case kSpec: return chain_fn<N, kSpec>(epi);
-        case kOrdered: return chain_fn<N, kOrdered>(epi);
-        case kNone: return chain_fn<N, kNone>(epi);
+        case kSpec: return chain_fn<N, kSpec>(epi, grouped);
+        case kOrdered: return chain_fn<N, kOrdered>(epi, grouped);
+        case kNone: return chain_fn<N, kNone>(epi, grouped);
     }
     return nullptr;
 }
 
-const void *chain_fn_any(int nranks, int mode, bool epi) {
+const void *chain_fn_any(int nranks, int mode, bool epi, bool grouped) {
     switch (nranks) {
-        case 1: return chain_fn_n<1>(mode, epi);
-        case 2: return chain_fn_n<2>(mode, epi);
-        case 3: return chain_fn_n<3>(mode, epi);
-        case 4: return chain_fn_n<4>(mode, epi);
-        case 5: return chain_fn_n<5>(mode, epi);
-        case 6: return chain_fn_n<6>(mode, epi);
-        case 7: return chain_fn_n<7>(mode, epi);
-        case 8: return chain_fn_n<8>(mode, epi);
+        case 1: return chain_fn_n<1>(mode, epi, grouped);
+        case 2: return chain_fn_n<2>(mode, epi, grouped);
+        case 3: return chain_fn_n<3>(mode, epi, grouped);
+        case 4: return chain_fn_n<4>(mode, epi, grouped);
+        case 5: return chain_fn_n<5>(mode, epi, grouped);
+        case 6: return chain_fn_n<6>(mode, epi, grouped);
+        case 7: return chain_fn_n<7>(mode, epi, grouped);
+        case 8: return chain_fn_n<8>(mode, epi, grouped);
     }
     return nullptr;
 }
@@ -690,22 +766,26 @@ hipError_t launch_reduce(const ReduceArgs &a, const ProduceArgs *next, int mode,
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_chain(const ChainArgs &a, int mode, bool epilogue, hipStream_t s) {
-    const void *fn = chain_fn_any(a.r.geo.nranks, mode, epilogue);
+hipError_t launch_chain(const ChainArgs &a, int mode, bool epilogue, int waves, hipStream_t s) {
+    if (waves != 1 && waves != kChainGroupWaves) return hipErrorInvalidValue;
+    const void *fn = chain_fn_any(a.r.geo.nranks, mode, epilogue, waves > 1);
     if (!fn) return hipErrorInvalidValue;
-    if (a.r.geo.segs != a.p.geo.segs || a.r.geo.tokens != a.p.geo.tokens)
+    if (a.r.geo.segs != a.p.geo.segs || a.r.geo.tokens != a.p.geo.tokens ||
+        a.r.geo.segs % waves != 0 || (waves > 1 && waves * a.r.geo.nranks > kLanes))
         return hipErrorInvalidValue;
-    const dim3 grid(static_cast<uint32_t>(a.r.geo.segs), static_cast<uint32_t>(a.r.geo.tokens), 2);
+    const dim3 grid(static_cast<uint32_t>(a.r.geo.segs / waves),
+                    static_cast<uint32_t>(a.r.geo.tokens), 2);
     void *args[] = {const_cast<ChainArgs *>(&a)};
-    return hipLaunchKernel(fn, grid, dim3(kLanes), args, 0, s);
+    return hipLaunchKernel(fn, grid, dim3(kLanes * waves), args, 0, s);
 }
 
 int max_active_groups(int nranks, int mode, bool epilogue, int waves_per_group) {
     return resident_groups(reduce_fn_any(nranks, mode, epilogue), waves_per_group * kLanes);
 }
 
-int max_active_chain_groups(int nranks, int mode, bool epilogue) {
-    return resident_groups(chain_fn_any(nranks, mode, epilogue), kLanes);
+int max_active_chain_groups(int nranks, int mode, bool epilogue, int waves) {
+    if (waves != 1 && waves != kChainGroupWaves) return 0;
+    return resident_groups(chain_fn_any(nranks, mode, epilogue, waves > 1), waves * kLanes);
 }
 
 hipError_t launch_advance(uint32_t *epoch_base, uint32_t step, hipStream_t s) {

@@ -12,6 +12,7 @@ constexpr int kVec = 8;                    // bf16 elements per 16-byte load
 constexpr int kChunk = kLanes * kVec;      // elements per chunk: one wave, one load per rank per lane
 constexpr int kMaxRanks = 8;
 constexpr int kMaxWavesPerGroup = 16;
+constexpr int kChainGroupWaves = 4;         // waves per persistent-step workgroup when grouped
 
 // Device-resident state shared by all kernels of a handle.
 struct DevState {
@@ -104,9 +105,13 @@ hipError_t launch_reduce(const ReduceArgs &a, const ProduceArgs *next, int mode,
 // Workgroups of the reduction kernel that can be resident at once on the
 // current device (0 if unknown).
 int max_active_groups(int nranks, int mode, bool epilogue, int waves_per_group);
-// Same for the one-wave workgroups of the persistent chain kernel.
-int max_active_chain_groups(int nranks, int mode, bool epilogue);
-hipError_t launch_chain(const ChainArgs &a, int mode, bool epilogue, hipStream_t s);
+// Same for the persistent chain kernel's workgroups of `waves` waves (1 or
+// kChainGroupWaves).
+int max_active_chain_groups(int nranks, int mode, bool epilogue, int waves);
+// Persistent step: grid (segs / waves, tokens, 2); waves = 1, or
+// kChainGroupWaves (segs divisible by it, waves * nranks <= 64) to let one
+// release fence cover a workgroup's chunks.
+hipError_t launch_chain(const ChainArgs &a, int mode, bool epilogue, int waves, hipStream_t s);
 hipError_t launch_advance(uint32_t *epoch_base, uint32_t step, hipStream_t s);
 hipError_t launch_set_base(uint32_t *epoch_base, uint32_t value, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t *p, uint32_t value, uint64_t count, hipStream_t s);

@@ -365,23 +365,27 @@ def test_persistent_many_steps_sampled():
     run.s.close()
 
 
+@pytest.mark.parametrize("T", [4, 8])
 @pytest.mark.parametrize("order", ["spec", "ordered"])
-def test_persistent_late_stamps(order):
+def test_persistent_late_stamps(order, T):
     """Late ranks' stamps land after a delay while the reduction waits on them:
-    outputs equal the oracle; the decision log shows retries and ends clean."""
+    outputs equal the oracle; the decision log shows retries and ends clean.
+    T = 8 (64 chunks) runs the grouped producer: one release fence and one
+    stamping wave per 4-chunk workgroup."""
     w = synth.SPEC_STRESS
     steps = 6
     late = synth.delay_table(w.wid, w.nranks, w.reduces_per_step * steps, w.stale_prob)
-    run = StepRun(w, 4, validate=order, persistent=1, late_delay=4)
+    run = StepRun(w, T, validate=order, persistent=1, late_delay=4)
     run.s.set_injection(inject_table(late))
     retried = 0
     for step in range(steps):
-        epochs = run.step(4)
+        print(f"late stamps {order} T={T} step {step}", flush=True)
+        epochs = run.step(T)
         got = to_host(run.out_d)
-        exp = oracle.reduce_chain(run.pool, epochs, 4)
+        exp = oracle.reduce_chain(run.pool, epochs, T)
         for i in range(w.reduces_per_step):
-            assert np.array_equal(got[i, :4], exp[i]), f"step={step} node={i}"
-        log = run.s.read_log()[:, :32]
+            assert np.array_equal(got[i, :T], exp[i]), f"step={step} node={i}"
+        log = run.s.read_log()[:, :T * 8]
         assert np.all((log >> 24) == 0)
         retried += int(np.count_nonzero((log & 0xFFFF) > 1))
     run.s.check()
@@ -389,13 +393,17 @@ def test_persistent_late_stamps(order):
     assert retried > 0
 
 
-def test_persistent_withheld_stamp_latches():
-    w = synth.Workload(70, "withheld", 4, (2,), 1024, 8, 1, "normal")
-    run = StepRun(w, 2, persistent=1, max_attempts=64, spin_limit=1 << 14)
+@pytest.mark.parametrize("T,H", [(2, 1024), (8, 4096)])
+def test_persistent_withheld_stamp_latches(T, H):
+    """A stamp that never lands ends the step with a latched error instead of
+    a hang; (8, 4096) is 64 chunks, the grouped producer."""
+    w = synth.Workload(70, "withheld", 4, (T,), H, 8, 1, "normal")
+    run = StepRun(w, T, persistent=1, max_attempts=64, spin_limit=1 << 14)
     table = [0] * 16
     table[4] = 0b0010 << 8      # epoch 5: rank 1's stamp never lands
     run.s.set_injection(table)
-    run.step(2)
+    print(f"withheld T={T} H={H}", flush=True)
+    run.step(T)
     assert run.s.status() == S.SIFAR_EDEVICE
     kind, epoch, chunk, attempts = run.s.error_info()
     assert kind in (S.SIFAR_DEV_RETRY_BUDGET, S.SIFAR_DEV_WAW)
@@ -418,6 +426,25 @@ def test_persistent_epilogue_moe_chain(T):
         for i in range(w.reduces_per_step):
             assert ulp_distance(y_got[i, :T], y_list[i]).max() <= 1, f"step {step} node {i}"
         res = r_list[-1]
+    run.s.check()
+    run.s.close()
+
+
+@pytest.mark.parametrize("N,T,H", [(5, 16, 3896), (8, 8, 4608), (3, 32, 2048)])
+def test_persistent_ragged_shapes(N, T, H):
+    """Persistent steps on shapes off the benchmark grid: 3896 leaves a partial
+    last chunk inside a grouped workgroup (8 chunks per token, 128 chunks);
+    4608 has 9 chunks per token, not divisible into 4-wave workgroups, so the
+    step falls back to one wave per workgroup; N = 3 with 64 chunks groups too."""
+    w = synth.Workload(73, f"ragged-{N}-{T}-{H}", N, (T,), H, 12, 1, "normal")
+    run = StepRun(w, T, persistent=1)
+    for rep in range(3):
+        print(f"ragged persistent N={N} T={T} H={H} rep {rep}", flush=True)
+        epochs = run.step(T)
+        got = to_host(run.out_d)
+        exp = oracle.reduce_chain(run.pool, epochs, T)
+        for i in range(w.reduces_per_step):
+            assert np.array_equal(got[i, :T], exp[i]), f"rep={rep} node={i}"
     run.s.check()
     run.s.close()
 
