@@ -54,7 +54,7 @@ def produce_bytes(N: int, T: int, H: int) -> int:
 
 def latency_floors() -> dict:
     """The library's latency probes (sifar_floor): launch and graph-node
-    floors, one agent-scope atomic, acquire / coherent / L2 / cache-missing
+    floors, one agent-scope atomic, acquire / coherent / warm / cache-missing
     load, a release fence after a store, and a release -> acquire handoff
     across and within an XCD."""
     import paper_2607_08973_amd as S
@@ -65,7 +65,7 @@ def latency_floors() -> dict:
         ("atomic_ns", S.SIFAR_FLOOR_ATOMIC, 4096, 1.0),
         ("acquire_load_ns", S.SIFAR_FLOOR_ACQUIRE_LOAD, 4096, 1.0),
         ("coherent_load_ns", S.SIFAR_FLOOR_COHERENT_LOAD, 4096, 1.0),
-        ("l2_load_ns", S.SIFAR_FLOOR_L2_LOAD, 4096, 1.0),
+        ("warm_load_ns", S.SIFAR_FLOOR_WARM_LOAD, 4096, 1.0),
         ("cold_load_ns", S.SIFAR_FLOOR_COLD_LOAD, 2048, 1.0),
         ("release_fence_ns", S.SIFAR_FLOOR_RELEASE_FENCE, 4096, 1.0),
         ("handoff_cross_xcd_ns", S.SIFAR_FLOOR_PINGPONG_XCD, 4096, 1.0),

@@ -267,8 +267,9 @@ const char *sifar_strerror(int code);
  *  ACQUIRE_LOAD      dependent agent-scope acquire loads of one word (a load
  *                    plus the L2 invalidate that acquire implies)
  *  COHERENT_LOAD     dependent agent-scope relaxed loads of one word
- *  L2_LOAD           dependent loads walking a 1 MiB ring line by line
- *                    (L2 hits: the ring does not fit the L1)
+ *  WARM_LOAD         dependent loads walking a 1 MiB ring that one pass has
+ *                    just read, a new 128-byte line each hop (more than the
+ *                    CU's L1 holds, far less than the XCD's L2)
  *  COLD_LOAD         dependent loads over a 1 GiB ring, each in a new line
  *                    and a new 4 MiB region, after the ring was pushed out of
  *                    L2 and the Infinity Cache (misses every cache and the
@@ -290,7 +291,7 @@ enum {
     SIFAR_FLOOR_ATOMIC = 2,
     SIFAR_FLOOR_ACQUIRE_LOAD = 3,
     SIFAR_FLOOR_COHERENT_LOAD = 4,
-    SIFAR_FLOOR_L2_LOAD = 5,
+    SIFAR_FLOOR_WARM_LOAD = 5,
     SIFAR_FLOOR_COLD_LOAD = 6,
     SIFAR_FLOOR_RELEASE_FENCE = 7,
     SIFAR_FLOOR_PINGPONG_XCD = 8,

@@ -47,7 +47,7 @@ SIFAR_FLOOR_EAGER_LAUNCH = 1
 SIFAR_FLOOR_ATOMIC = 2
 SIFAR_FLOOR_ACQUIRE_LOAD = 3
 SIFAR_FLOOR_COHERENT_LOAD = 4
-SIFAR_FLOOR_L2_LOAD = 5
+SIFAR_FLOOR_WARM_LOAD = 5
 SIFAR_FLOOR_COLD_LOAD = 6
 SIFAR_FLOOR_RELEASE_FENCE = 7
 SIFAR_FLOOR_PINGPONG_XCD = 8

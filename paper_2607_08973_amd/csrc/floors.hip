@@ -1,8 +1,8 @@
 // Latency floors of one MI355X, the yardsticks the all-reduce's latency is read
 // against: what a graph node, an eager launch, an agent-scope atomic, an
-// acquire load, a coherent load, an L2 hit, a load that misses every cache, an
-// agent-scope release fence and a release -> acquire handoff between two XCDs
-// cost on their own.
+// acquire load, a coherent load, a load of recently read data, a load that
+// misses every cache, an agent-scope release fence and a release -> acquire
+// handoff between two XCDs cost on their own.
 //
 // Each device-side probe is one wave whose lane 0 runs a chain of dependent
 // operations (every address depends on the previous result, so the operations
@@ -265,11 +265,11 @@ extern "C" int sifar_floor(int32_t kind, int32_t iterations, void *stream, doubl
         rc = launch_ok();
         break;
     }
-    case SIFAR_FLOOR_L2_LOAD:
+    case SIFAR_FLOOR_WARM_LOAD:
     case SIFAR_FLOOR_COLD_LOAD: {
-        // L2: a 1 MiB ring (more than the CU's L1, less than the XCD's L2)
-        // walked line after line, so address translation stays warm; warmed
-        // by one pass. Cold: a 1 GiB ring walked 4 MiB + 4224 B at a time,
+        // Warm: a 1 MiB ring (more than the CU's L1, less than the XCD's L2)
+        // walked line after line, so address translation stays warm, after
+        // one pass over it. Cold: a 1 GiB ring walked 4 MiB + 4224 B at a time,
         // every hop a new line and a new translation, after 512 MiB of
         // unrelated writes have pushed it out of L2 and the Infinity Cache.
         const bool cold = kind == SIFAR_FLOOR_COLD_LOAD;

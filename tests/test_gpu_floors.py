@@ -18,7 +18,7 @@ KINDS = [
     (S.SIFAR_FLOOR_ATOMIC, 4096),
     (S.SIFAR_FLOOR_ACQUIRE_LOAD, 4096),
     (S.SIFAR_FLOOR_COHERENT_LOAD, 4096),
-    (S.SIFAR_FLOOR_L2_LOAD, 4096),
+    (S.SIFAR_FLOOR_WARM_LOAD, 4096),
     (S.SIFAR_FLOOR_COLD_LOAD, 1024),
     (S.SIFAR_FLOOR_RELEASE_FENCE, 4096),
     (S.SIFAR_FLOOR_PINGPONG_XCD, 2048),
@@ -49,7 +49,8 @@ def test_floor_probe_completes(kind, iterations):
 
 
 def test_floors_order():
-    """A cache-missing load costs more than an L2 hit."""
-    l2, _ = S.sifar_floor(S.SIFAR_FLOOR_L2_LOAD, 4096)
+    """A load that misses every cache costs more than one of recently read
+    data."""
+    warm, _ = S.sifar_floor(S.SIFAR_FLOOR_WARM_LOAD, 4096)
     cold, _ = S.sifar_floor(S.SIFAR_FLOOR_COLD_LOAD, 1024)
-    assert cold > l2, (cold, l2)
+    assert cold > warm, (cold, warm)
