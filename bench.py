@@ -151,7 +151,7 @@ def parse():
     ap.add_argument("--floor-nodes", type=int, default=64)
     ap.add_argument("--workload", default="llama8b-decode",
                     choices=["llama8b-decode", "smoke-n2", "spec-stress", "sweep", "moe-rmsnorm",
-                             "ablation", "retry-curve"],
+                             "ablation", "retry-curve", "reduce-cold"],
                     help="llama8b-decode is the headline line; the others print one "
                          "JSON line per configuration")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -285,10 +285,62 @@ def chain_point(w, T, args, *, T_max=None, pool_entries=None, inject=False, wave
     return out
 
 
+def reduce_point(w, args, scrub, reps=30):
+    """One eager all-reduce (the plain reduction kernel, no peers in its
+    launch), `reps` rounds warm (reduce right after its producer) and `reps`
+    rounds cold (a 512 MiB write between producer and reduce pushes the slots
+    out of L2 and the Infinity Cache). Event times here are per round (the
+    producer and the scrub included); the reduction kernel's own duration in
+    each condition comes from a kernel trace of this workload (in a trace, a
+    cold reduce is the one dispatched right after the scrub's fill kernel)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2607_08973_amd as S
+    import synth
+
+    N, T, H = w.nranks, w.tokens[0], w.hidden
+    P = 3
+    pool = synth.payload_pool(w.wid, N, T, H, P, w.dist)
+    src = torch.from_numpy(pool.view(np.int16)).to("cuda:0")
+    out = torch.zeros((T, H), dtype=torch.int16, device="cuda:0")
+    res = {"workload": "reduce-" + w.name, "nranks": N, "tokens": T, "hidden": H,
+           "reduce_bytes": reduce_bytes(N, T, H), "reps": reps}
+    with S.Sifar(nranks=N, hidden=H, max_tokens=T, reduces_per_step=2, validate=args.mode,
+                 log_epochs=8) as s:
+        s.produce(src[0], T)
+        s.reduce(out, T)
+        for kind in ("warm", "cold"):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record()
+            for k in range(reps):
+                s.produce(src[k % P], T)
+                if kind == "cold":
+                    scrub.fill_(k & 0x7F)
+                s.reduce(out, T)
+            b.record()
+            torch.cuda.synchronize()
+            res[f"{kind}_round_us"] = a.elapsed_time(b) * 1e3 / reps
+        s.check()
+        assert np.array_equal(out.cpu().numpy().view(np.uint16),
+                              oracle.reduce(pool[(reps - 1) % P])), f"{w.name}: output != oracle"
+    return res
+
+
 def suite(args):
     """Secondary workloads: one JSON line each (not the headline metric)."""
     import synth
 
+    if args.workload == "reduce-cold":
+        import torch
+        scrub = torch.empty(512 << 20, dtype=torch.uint8, device="cuda:0")
+        for w in synth.PAYLOAD_SWEEP:
+            p = reduce_point(w, args, scrub)
+            print(json.dumps({k: (round(v, 4) if isinstance(v, float) else v)
+                              for k, v in p.items()}), flush=True)
+        return
     if args.workload == "smoke-n2":
         pts = [chain_point(synth.SMOKE_N2, 1, args)]
     elif args.workload == "spec-stress":

@@ -249,12 +249,24 @@ def test_pairs_on_gpu_against_oracle():
         s.check()
 
 
-@pytest.mark.parametrize("N,T,H", [(8, 256, 8192), (2, 256, 4096), (4, 64, 8192)])
-def test_payload_sweep_largest_points(N, T, H):
-    """The largest payloads of the latency-to-bandwidth sweep (up to 4 MiB per
-    rank), U(-1, 1) values, full outputs for 3 reduces."""
+SWEEP_POINTS = [(w.nranks, w.tokens[0], w.hidden) for w in synth.PAYLOAD_SWEEP]
+
+
+@pytest.mark.parametrize("persistent", [0, 1])
+@pytest.mark.parametrize("N,T,H", SWEEP_POINTS)
+def test_payload_sweep_points(N, T, H, persistent):
+    """Every point of the latency-to-bandwidth sweep (8 KiB to 4 MiB per rank),
+    U(-1, 1) values, full outputs of a 4-reduce step, per-launch and
+    persistent (where the persistent step fits the GPU)."""
     w = synth.Workload(4, f"sweep-n{N}-t{T}-h{H}", N, (T,), H, 4, 1, "uniform")
-    run = StepRun(w, T, pool=synth.payload_pool(4, N, T, H, 5, "uniform"))
+    print(f"sweep N={N} T={T} H={H} persistent={persistent}", flush=True)
+    try:
+        run = StepRun(w, T, pool=synth.payload_pool(4, N, T, H, 5, "uniform"),
+                      persistent=persistent)
+    except S.SifarError as e:
+        if persistent and e.code == S.SIFAR_EINVAL:
+            pytest.skip("the persistent step needs more co-resident waves than the GPU holds")
+        raise
     epochs = run.step(T)
     got = to_host(run.out_d)
     for i in range(0, 4):
