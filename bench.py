@@ -154,6 +154,8 @@ def parse():
                              "ablation", "retry-curve", "reduce-cold"],
                     help="llama8b-decode is the headline line; the others print one "
                          "JSON line per configuration")
+    ap.add_argument("--wpg", type=int, default=1, choices=[1, 2, 4, 8, 16],
+                    help="reduce-cold: waves per workgroup of the reduction kernel")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline (0 disables it)")
     return ap.parse_args()
@@ -306,9 +308,9 @@ def reduce_point(w, args, scrub, reps=30):
     src = torch.from_numpy(pool.view(np.int16)).to("cuda:0")
     out = torch.zeros((T, H), dtype=torch.int16, device="cuda:0")
     res = {"workload": "reduce-" + w.name, "nranks": N, "tokens": T, "hidden": H,
-           "reduce_bytes": reduce_bytes(N, T, H), "reps": reps}
+           "reduce_bytes": reduce_bytes(N, T, H), "reps": reps, "waves_per_group": args.wpg}
     with S.Sifar(nranks=N, hidden=H, max_tokens=T, reduces_per_step=2, validate=args.mode,
-                 log_epochs=8) as s:
+                 log_epochs=8, waves_per_group=args.wpg) as s:
         s.produce(src[0], T)
         s.reduce(out, T)
         for kind in ("warm", "cold"):
@@ -329,6 +331,39 @@ def reduce_point(w, args, scrub, reps=30):
     return res
 
 
+def torch_sum_reference(w, scrub, reps=30):
+    """PyTorch's own reduction over the rank dimension (x.sum(0) on bf16 with
+    fp32 accumulation: the same N reads and one write) at one sweep shape,
+    warm and cold like reduce_point, for the kernel trace to compare with."""
+    import numpy as np
+    import torch
+
+    import synth
+
+    N, T, H = w.nranks, w.tokens[0], w.hidden
+    pool = synth.payload_pool(w.wid, N, T, H, 3, w.dist)
+    src = torch.from_numpy(pool.view(np.int16)).to("cuda:0").view(torch.bfloat16)
+    x = torch.empty((N, T * H), dtype=torch.bfloat16, device="cuda:0")
+    res = {"workload": "torch-sum-" + w.name, "nranks": N, "tokens": T, "hidden": H,
+           "reduce_bytes": reduce_bytes(N, T, H), "reps": reps}
+    x.copy_(src[0].reshape(N, T * H))
+    y = x.sum(0)  # first call outside the timed rounds
+    for kind in ("warm", "cold"):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for k in range(reps):
+            x.copy_(src[k % 3].reshape(N, T * H))
+            if kind == "cold":
+                scrub.fill_(k & 0x7F)
+            y = x.sum(0)
+        b.record()
+        torch.cuda.synchronize()
+        res[f"{kind}_round_us"] = a.elapsed_time(b) * 1e3 / reps
+    del y
+    return res
+
+
 def suite(args):
     """Secondary workloads: one JSON line each (not the headline metric)."""
     import synth
@@ -336,8 +371,9 @@ def suite(args):
     if args.workload == "reduce-cold":
         import torch
         scrub = torch.empty(512 << 20, dtype=torch.uint8, device="cuda:0")
-        for w in synth.PAYLOAD_SWEEP:
-            p = reduce_point(w, args, scrub)
+        pts = [reduce_point(w, args, scrub) for w in synth.PAYLOAD_SWEEP]
+        pts.append(torch_sum_reference(synth.PAYLOAD_SWEEP[-1], scrub))
+        for p in pts:
             print(json.dumps({k: (round(v, 4) if isinstance(v, float) else v)
                               for k, v in p.items()}), flush=True)
         return
