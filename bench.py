@@ -140,7 +140,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--mode", default="spec", choices=["spec", "ordered", "none"])
+    ap.add_argument("--mode", default=None, choices=["spec", "ordered", "none"],
+                    help="validation; default: ordered for persistent steps (the only "
+                         "mode they accept), spec for one launch per all-reduce")
     ap.add_argument("--fuse", type=int, default=1, choices=[0, 1],
                     help="1: the peers' next write shares the reduction's launch")
     ap.add_argument("--persistent", type=int, default=1, choices=[0, 1],
@@ -158,7 +160,14 @@ def parse():
                     help="reduce-cold: waves per workgroup of the reduction kernel")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline (0 disables it)")
-    return ap.parse_args()
+    args = ap.parse_args()
+    steps_persistent = args.persistent and args.workload not in ("ablation", "reduce-cold")
+    if args.mode is None:
+        args.mode = "ordered" if steps_persistent else "spec"
+    if steps_persistent and args.mode != "ordered":
+        raise SystemExit("persistent steps validate before they load: use --mode ordered "
+                         "(or --persistent 0 for spec / none)")
+    return args
 
 
 def cpu_baseline(pool, tokens, budget_s):
@@ -388,11 +397,12 @@ def suite(args):
         # the paper's incremental optimisations (Sec. 6.3) as they exist here:
         # one buffer (bottom barrier) -> dual buffering; ORDERED (top barrier by
         # flag polling) -> SPEC (speculative); NONE = the "no barrier" ideal.
+        # Persistent steps run ORDERED only (they validate before they load).
         import copy
         w = synth.LLAMA8B_DECODE
         pts = []
         combos = [(p_, b, m) for p_ in (0, 1) for b in (1, 2) for m in ("ordered", "spec", "none")
-                  if not (p_ and m == "none")]
+                  if not (p_ and m != "ordered")]
         for p_, b, m in combos:
             a2 = copy.copy(args)
             a2.persistent, a2.buffers, a2.mode = p_, b, m
@@ -557,7 +567,7 @@ def main():
     del calib, calib_dst
 
     traffic = None
-    if args.mode == "spec" and args.buffers == 2 and args.persistent:
+    if args.mode == "ordered" and args.buffers == 2 and args.persistent:
         traffic = measured_traffic("persistent")
     elif args.mode == "spec" and args.buffers == 2 and args.fuse:
         traffic = measured_traffic("fused")

@@ -77,11 +77,17 @@ typedef struct sifar_ctx *sifar_t;
  *          stamps are loaded together, validation follows, a stale stamp
  *          re-runs both. Correct when a rank whose stamp is fresh at
  *          validation also had its payload in place when it was loaded -- the
- *          monotonicity assumption of Sec. 8.1.
- * ORDERED  stamps are acquired first and the payload is loaded only once all
+ *          monotonicity assumption of Sec. 8.1. It holds for the per-epoch
+ *          launches (eager calls, step graphs with persistent = 0): every
+ *          epoch's payload was written by an earlier launch. It does not hold
+ *          for a producer that is writing at that moment: measured on MI355X
+ *          with producer and consumer on different XCDs, ~2 % of persistent
+ *          all-reduces accepted a rank's previous epoch under a fresh stamp.
+ *          So persistent steps refuse SPEC (SIFAR_EINVAL).
+ * ORDERED  stamps are read first and the payload is loaded only once all
  *          are fresh: a top barrier by flag polling (the "oneshot + dual
  *          buffering" configuration of Sec. 3.4). Correct without any
- *          monotonicity assumption.
+ *          monotonicity assumption; the only mode of persistent steps.
  * NONE     no stamps are read: the idealised "no barrier" configuration of
  *          Sec. 6.3. Only correct when stream order alone guarantees the data,
  *          so not allowed with persistent steps. */
@@ -120,7 +126,8 @@ typedef struct {
     int32_t persistent;       /* step graphs: 1 = one persistent launch runs the whole step, its
                                  consumer waves and the emulated peers' waves synchronising
                                  through stamps in flight (a megakernel-style chain, Sec. 5);
-                                 needs 2 x max_tokens x ceil(hidden / 512) co-resident waves */
+                                 needs validate = ORDERED and 2 x max_tokens x
+                                 ceil(hidden / 512) co-resident waves */
     uint32_t late_delay;      /* persistent steps with injection: a late rank's stamp lands
                                  this many ~0.2 us sleeps after its payload */
     int32_t buffers;          /* 2: dual buffering (Sec. 3.3; no bottom barrier). 1: one slot per
@@ -208,9 +215,10 @@ int sifar_bind_step(sifar_t h, const sifar_step_buffers *b);
  * produce(g1), then L-1 launches that each reduce g_i while writing g_(i+1),
  * then reduce(g_L): L + 1 kernel nodes; without it, L x (produce, reduce);
  * with persistent, one launch for the whole step. In a persistent step the
- * peers run concurrently with the reduction, so mis-speculation happens for
- * real (the decision log records it) and injected late stamps land after
- * late_delay instead of after the first failed validation.
+ * peers run concurrently with the reduction, so a reduction often reaches an
+ * epoch before its stamps (the decision log records the polls: attempts and
+ * the stale ranks of the first and last poll), and injected late stamps land
+ * after late_delay instead of after the first failed validation.
  * The graph for a token count is captured on first use (on a library-owned
  * stream) and replayed afterwards; epochs and parities come from a
  * device-resident counter, so a replay needs no host work. Requires no

@@ -27,6 +27,7 @@ struct sifar_ctx {
     uint32_t *produced = nullptr;  // [2][w_max]
     uint32_t *log = nullptr;       // [log_epochs][w_max]
     uint64_t *exch = nullptr;      // [2][max_tokens][exch_q]
+    uint64_t *place = nullptr;     // [2][w_max] XCD tags of each chunk's consumer / producer
     int exch_q = 1;                // exchange words per token and parity
     DevState *state = nullptr;
     uint16_t *inject = nullptr;
@@ -74,8 +75,12 @@ int check_cfg(const sifar_config *c) {
     if (c->fuse_peers != 0 && c->fuse_peers != 1) return SIFAR_EINVAL;
     if (c->persistent != 0 && c->persistent != 1) return SIFAR_EINVAL;
     if (c->buffers != 1 && c->buffers != 2) return SIFAR_EINVAL;
-    // a live step without validation would read peers' slots mid-write
-    if (c->persistent && c->validate == SIFAR_VALIDATE_NONE) return SIFAR_EINVAL;
+    // A persistent step reads slots its peers are writing at that moment. Only
+    // ORDERED is sound there: without validation the reads race the writes,
+    // and speculative loads issued with the stamp loads were measured to
+    // return a rank's previous epoch while its stamp already read fresh (the
+    // monotonicity the paper assumes, Sec. 8.1, does not hold across XCDs).
+    if (c->persistent && c->validate != SIFAR_VALIDATE_ORDERED) return SIFAR_EINVAL;
     return SIFAR_OK;
 }
 
@@ -202,6 +207,7 @@ int capture_step(sifar_t h, int32_t tokens, hipGraphExec_t *out) {
         ca.epoch_base = &h->state->epoch_base;
         ca.advance = advance;
         ca.done = &h->state->chain_done;
+        ca.place = h->place;
         ca.parity_mask = parity_mask(h);
         rc = hip_status(launch_chain(ca, h->cfg.validate, h->cfg.epilogue != 0, waves, s));
     } else if (h->cfg.fuse_peers && h->cfg.buffers == 2) {
@@ -324,6 +330,7 @@ int sifar_init(const sifar_config *cfg, sifar_t *out) {
     if (!rc) rc = dev_alloc(&h->produced, static_cast<size_t>(2) * h->w_max);
     if (!rc) rc = dev_alloc(&h->log, static_cast<size_t>(c.log_epochs) * h->w_max);
     if (!rc) rc = dev_alloc(&h->exch, static_cast<size_t>(2) * c.max_tokens * h->exch_q);
+    if (!rc) rc = dev_alloc(&h->place, static_cast<size_t>(2) * h->w_max);
     if (!rc) rc = dev_alloc(&h->state, 1);
     if (!rc && hipStreamCreateWithFlags(&h->capture, hipStreamNonBlocking) != hipSuccess)
         rc = SIFAR_EHIP;
@@ -340,6 +347,9 @@ int sifar_init(const sifar_config *cfg, sifar_t *out) {
         if (e == hipSuccess)
             e = launch_fill_u32(reinterpret_cast<uint32_t *>(h->exch), 0,
                                 static_cast<uint64_t>(2) * c.max_tokens * h->exch_q * 2, s);
+        if (e == hipSuccess)
+            e = launch_fill_u32(reinterpret_cast<uint32_t *>(h->place), 0,
+                                static_cast<uint64_t>(2) * h->w_max * 2, s);
         if (e == hipSuccess)
             e = launch_fill_u32(reinterpret_cast<uint32_t *>(h->state), 0,
                                 sizeof(DevState) / sizeof(uint32_t), s);
@@ -365,6 +375,7 @@ void sifar_destroy(sifar_t h) {
     (void)hipFree(h->produced);
     (void)hipFree(h->log);
     (void)hipFree(h->exch);
+    (void)hipFree(h->place);
     (void)hipFree(h->state);
     (void)hipFree(h->inject);
     delete h;

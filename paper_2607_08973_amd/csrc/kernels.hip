@@ -107,6 +107,7 @@ __device__ void latch(uint32_t *err, uint32_t kind, uint32_t g, uint32_t c, uint
 __device__ __forceinline__ bool latched(const uint32_t *err) { return ld_relaxed(err) != 0; }
 
 constexpr uint32_t kErrRetryBudget = 1, kErrWaw = 2, kErrExchange = 3;
+constexpr uint32_t kPlaceSpins = 1u << 14;  // polls for a partner wave's placement tag
 
 // Where the calling lane works: token t, chunk s of the row, chunk index c.
 // Lanes past the end of the row load a clamped, in-bounds address and do not
@@ -154,6 +155,62 @@ __device__ __forceinline__ void copy_chunk(const ProduceArgs &a, const Chunk &k,
     if (k.lane_ok) {
 #pragma unroll
         for (int r = 0; r < N; ++r) st16(dst + r * 2 * geo.slot_elems, v[r]);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Placement of a persistent step's waves. Workgroups are dealt to the 8 XCDs
+// round robin, so a chunk's consumer and producer share an XCD when the
+// plane offset is a multiple of 8 -- but the kernel reads where it runs
+// (XCC_ID) instead of assuming it. At step start every wave publishes
+// ((base + 1) << 32) | 0x100 | XCD for its chunk and plane; a wave then reads
+// its partner's tag (bounded wait; a missing tag counts as another XCD).
+
+__device__ __forceinline__ uint32_t xcc_id() {
+    uint32_t v;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(v));
+    return v;
+}
+
+__device__ __forceinline__ uint64_t place_tag(uint32_t base, uint32_t xcc) {
+    return (static_cast<uint64_t>(base + 1u) << 32) | 0x100u | xcc;
+}
+
+__device__ __forceinline__ void publish_place(uint64_t *place, uint32_t base, int lane) {
+    if (lane == 0)
+        __hip_atomic_store(place, place_tag(base, xcc_id()), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Wave-uniform: does the partner wave whose tag is *place run on this XCD?
+__device__ __forceinline__ bool partner_is_local(const uint64_t *place, uint32_t base, int lane) {
+    uint32_t local = 0;
+    if (lane == 0) {
+        const uint64_t want = place_tag(base, xcc_id());
+        uint64_t t = 0;
+        for (uint32_t spins = 0; spins < kPlaceSpins; ++spins) {
+            t = __hip_atomic_load(place, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if ((t >> 32) == (want >> 32)) break;
+            __builtin_amdgcn_s_sleep(1);
+        }
+        local = t == want ? 1u : 0u;
+    }
+    return __builtin_amdgcn_readfirstlane(local) != 0;
+}
+
+// Publication of a producer's slot stores before its stamps. To a consumer on
+// another XCD: an agent-scope release fence, which writes back this XCD's L2.
+// To a consumer on this XCD: waiting until the stores have reached the L2 is
+// enough, because the L2 is the point of coherence of all CUs of one XCD and
+// the consumer's agent-scope loads bypass its CU's L1 (the threadgroup-split
+// workgroup scope of the LLVM AMDGPU memory model rests on the same fact: its
+// release waits for the stores, its acquire bypasses or invalidates L1).
+__device__ __forceinline__ void publish_slot(bool local) {
+    if (local) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    } else {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     }
 }
 
@@ -217,10 +274,16 @@ __device__ __forceinline__ void load_payload(V16 (&v)[N], const uint16_t *slot0,
 // AGENT: payload through agent-scope loads (persistent chain), stamps first.
 // INJECT_HOOK: deterministic injection, the late ranks' stamps land right
 // after the first failed validation (only when producers have finished).
+// AGENT: a persistent step, whose producer may be writing right now. There
+// only ORDERED is sound: the stamps are polled with relaxed agent-scope loads,
+// and the payload is loaded once every stamp is fresh -- after an acquire
+// fence when the chunk's producer is on another XCD (`local` false), directly
+// when it shares this XCD (see publish_slot).
 template <int N, int MODE, bool AGENT, bool INJECT_HOOK>
 __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint32_t g, uint32_t p,
                                        int lane, V16 (&v)[N], uint32_t &attempts, uint32_t &first,
-                                       uint32_t &last) {
+                                       uint32_t &last, bool local = false) {
+    static_assert(!AGENT || MODE == kOrdered, "a persistent step validates before it loads");
     const Geometry &geo = a.geo;
     const uint16_t *slot0 = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + k.row;
     const uint64_t rank_step = 2 * geo.slot_elems;  // slots are [rank][parity]
@@ -228,10 +291,7 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
 
     uint32_t st = 0;
     if (MODE == kOrdered) {
-        if (k.active && lane < N) st = ld_acquire(stamp + lane);
-    } else if (AGENT) {
-        if (MODE == kSpec && k.active && lane < N) st = ld_relaxed(stamp + lane);
-        load_payload<N, AGENT>(v, slot0, rank_step);
+        if (k.active && lane < N) st = AGENT ? ld_relaxed(stamp + lane) : ld_acquire(stamp + lane);
     } else {
         load_payload<N, AGENT>(v, slot0, rank_step);
         if (MODE == kSpec && k.active && lane < N) st = ld_relaxed(stamp + lane);
@@ -258,10 +318,10 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
                 __builtin_amdgcn_s_sleep(1);  // a live peer is still writing
             }
             // Plain reloads need an acquire fence (an L2 invalidate) to see the
-            // peers' data; agent-scope reloads are coherent without one.
+            // peers' data; the persistent step polls stamps only.
             if (!AGENT) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             if (MODE == kOrdered) {
-                if (lane < N) st = ld_acquire(stamp + lane);
+                if (lane < N) st = AGENT ? ld_relaxed(stamp + lane) : ld_acquire(stamp + lane);
             } else {
                 if (lane < N) st = ld_relaxed(stamp + lane);
                 load_payload<N, AGENT>(v, slot0, rank_step);
@@ -272,7 +332,15 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
             fail = m != 0 || attempts <= a.forced_retries;
         }
     }
-    if (MODE == kOrdered) load_payload<N, AGENT>(v, slot0, rank_step);
+    if (MODE == kOrdered) {
+        if (AGENT) {
+            if (local)
+                __atomic_signal_fence(__ATOMIC_SEQ_CST);
+            else
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        }
+        load_payload<N, AGENT>(v, slot0, rank_step);
+    }
 }
 
 // Fixed-order fp32 sum: acc = x_0; acc += x_1; ... acc += x_{N-1}; then bf16.
@@ -429,27 +497,34 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
 // Per chunk and epoch g of parity p:
 //   producer  wait until consumed[p] == produced[p] (the reduction that read
 //             this slot two epochs back has finished: dual buffering), copy
-//             the N partials, agent-scope release fence, store the on-time
+//             the N partials, publish them (publish_slot: a release fence
+//             only when the consumer is on another XCD), store the on-time
 //             stamps and produced[p] = g; injected late ranks' stamps follow
 //             after `late_delay` sleeps.
-//   consumer  stamps, then payload, through agent-scope loads (SPEC; ORDERED
-//             acquires the stamps first); retry with backoff while stale;
-//             sum; store; consumed[p] = g once every payload load has
-//             completed.
+//   consumer  poll the stamps (relaxed agent-scope loads, backoff) until all
+//             are fresh, then load the payload (after an acquire fence when
+//             the producer is on another XCD); sum; store; consumed[p] = g
+//             once every payload load has completed.
+// Validation comes before the payload loads here (ORDERED). Speculative
+// payload loads issued alongside the stamp loads were measured to return a
+// rank's previous epoch while its stamp already read as fresh when producer
+// and consumer sat on different XCDs: the monotonicity the paper assumes
+// (Sec. 8.1) does not hold for a live producer on MI355X. (The per-epoch
+// launches keep SPEC: there every epoch was written by an earlier launch.)
 // The producer can run one epoch ahead of the consumer, no further.
 // Producer wave of chunk (t, s), one epoch after the other: wait until the
 // slot of this parity is free (with a single buffer: until the previous
-// epoch's reduction is done -- the bottom barrier), copy, one agent-scope
-// release fence, stamps.
+// epoch's reduction is done -- the bottom barrier), copy, publish, stamps.
 // (Measured on MI355X: prefetching the next epoch's sources or batching
-// several chunks per wave behind one fence makes the step slower -- the
-// consumer then reaches each epoch before its stamps and pays a retry, and the
+// several chunks per wave behind one fence does not shorten the step -- the
 // dual-buffer rule ties the producer of g + 1 to the reduction of g - 1.)
 template <int N, int MODE, bool EPI>
 __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base, int lane) {
     const ProduceArgs &a = A.p;
     const Geometry &geo = a.geo;
     const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x, lane);
+    publish_place(A.place + geo.w_max + k.c, base, lane);
+    const bool local = partner_is_local(A.place + k.c, base, lane);
     for (int i = 0; i < A.reduces; ++i) {
         const uint32_t g = base + static_cast<uint32_t>(i) + 1u;
         const uint32_t p = static_cast<uint32_t>(i + 1) & A.parity_mask;
@@ -467,7 +542,7 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
         }
         copy_chunk<N>(a, k, g, p);
         const uint32_t held = held_back(a.inject, a.inject_entries, g);
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        publish_slot(local);
         uint32_t *stamp = a.stamps + pc * N;
         if (lane < N && !((held >> lane) & 1u)) st_relaxed(stamp + lane, g);
         if (lane == 0) st_relaxed(a.produced + pc, g);
@@ -481,10 +556,11 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
 }
 
 // Grouped producer (G waves per workgroup, one chunk per wave): the waves
-// copy their chunks, meet at a workgroup barrier, and wave 0 issues ONE
-// agent-scope release fence for all of them and stores every chunk's stamps
-// (lane = chunk wave * N + rank). An agent-scope release writes back the XCD's
-// L2 and fences of one XCD serialise, so sharing one fence among G chunks
+// copy their chunks, wait until their stores have reached L2, meet at a
+// workgroup barrier, and wave 0 publishes for all of them (one agent-scope
+// release fence, needed only when a consumer of the group is on another XCD)
+// and stores every chunk's stamps (lane = chunk wave * N + rank). Such fences
+// write back the XCD's L2 and serialise per XCD, so sharing one among G chunks
 // shortens the epoch once several producer waves share each XCD. Every wave
 // reaches the barrier in every epoch; a failed slot wait ends the whole
 // workgroup at the same barrier.
@@ -497,6 +573,9 @@ __device__ __forceinline__ void chain_producer_grouped(const ChainArgs &A, uint3
     const int sw = lane / N, sr = lane - sw * N;
     const Chunk ks = chunk_at(geo, blockIdx.y, blockIdx.x * G + (sw < G ? sw : 0), 0);
     const bool stamper = wave == 0 && sw < G && ks.active;
+    if (k.active) publish_place(A.place + geo.w_max + k.c, base, lane);
+    const bool mine = !k.active || partner_is_local(A.place + k.c, base, lane);
+    const bool local = __syncthreads_and(mine ? 1 : 0) != 0;
     for (int i = 0; i < A.reduces; ++i) {
         const uint32_t g = base + static_cast<uint32_t>(i) + 1u;
         const uint32_t p = static_cast<uint32_t>(i + 1) & A.parity_mask;
@@ -523,7 +602,7 @@ __device__ __forceinline__ void chain_producer_grouped(const ChainArgs &A, uint3
         if (__syncthreads_or(!free)) return;
         if (wave == 0) {
             const uint32_t held = held_back(a.inject, a.inject_entries, g);
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+            publish_slot(local);  // with `local` the wait above already did it
             const size_t ps = static_cast<size_t>(p) * geo.w_max + ks.c;
             uint32_t *stamp = a.stamps + ps * N;
             if (stamper && !((held >> sr) & 1u)) st_relaxed(stamp + sr, g);
@@ -545,6 +624,8 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
     const ReduceArgs &a = A.r;
     const Geometry &geo = a.geo;
     const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x * G + wave, lane);
+    if (k.active) publish_place(A.place + k.c, base, lane);
+    const bool local = k.active && partner_is_local(A.place + geo.w_max + k.c, base, lane);
     V16 wv;
     if (EPI) wv = ld16(a.weight + k.elem);
     for (int i = 0; i < A.reduces; ++i) {
@@ -554,7 +635,7 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
         if (EPI) rv = ld16(a.residual + k.row);  // this wave's own previous store
         V16 v[N];
         uint32_t attempts, first, last;
-        gather<N, MODE, true, false>(a, k, g, p, lane, v, attempts, first, last);
+        gather<N, MODE, true, false>(a, k, g, p, lane, v, attempts, first, last, local);
         const V16 o = sum_round<N>(v);
         complete(o);  // every payload load has returned before the slot is released
         if (lane == 0) {
@@ -660,14 +741,10 @@ const void *chain_fn(bool epi, bool grouped) {
                : reinterpret_cast<const void *>(chain_kernel<N, MODE, false, false>);
 }
 
+// Persistent steps validate before they load: ORDERED only.
 template <int N>
 const void *chain_fn_n(int mode, bool epi, bool grouped) {
-    switch (mode) {
-        case kSpec: return chain_fn<N, kSpec>(epi, grouped);
-        case kOrdered: return chain_fn<N, kOrdered>(epi, grouped);
-        case kNone: return chain_fn<N, kNone>(epi, grouped);
-    }
-    return nullptr;
+    return mode == kOrdered ? chain_fn<N, kOrdered>(epi, grouped) : nullptr;
 }
 
 const void *chain_fn_any(int nranks, int mode, bool epi, bool grouped) {

@@ -94,6 +94,8 @@ struct ChainArgs {
     uint32_t advance;
     uint32_t *done;              // arrival counter of the step's waves (left at 0)
     uint32_t parity_mask;        // 1: dual buffering (parity = epoch & 1); 0: one slot
+    uint64_t *place;             // [2][w_max]: plane 0 consumer, plane 1 producer of each
+                                 // chunk: (base + 1) << 32 | 0x100 | XCD, written at step start
 };
 
 enum Mode : int { kSpec = 0, kOrdered = 1, kNone = 2 };

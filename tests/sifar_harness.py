@@ -43,8 +43,12 @@ def expected_log_words(nranks, late_masks_by_epoch, order, forced=0):
 class StepRun:
     """A handle bound to a device-resident source pool and output ring."""
 
-    def __init__(self, w: synth.Workload, tokens_max: int, validate="spec", log_epochs=None,
+    def __init__(self, w: synth.Workload, tokens_max: int, validate=None, log_epochs=None,
                  waves_per_group=1, pool=None, **cfg):
+        # persistent steps validate before they load (ORDERED); per-epoch
+        # launches default to the paper's speculative reduction
+        if validate is None:
+            validate = "ordered" if cfg.get("persistent") else "spec"
         self.w = w
         self.N, self.H, self.L = w.nranks, w.hidden, w.reduces_per_step
         self.T_max = tokens_max

@@ -71,12 +71,17 @@ def test_invalid_config_rejected_on_host(field, value):
     assert rc == S.SIFAR_EINVAL and not h.value
 
 
-def test_persistent_without_validation_rejected():
+@pytest.mark.parametrize("mode", [0, 2])  # SPEC, NONE
+def test_persistent_step_requires_ordered_validation(mode):
+    """A persistent step reads slots its peers are writing: without validation
+    the reads race the writes, and speculative loads were measured to return
+    stale ranks whose stamps read fresh; only ORDERED is accepted."""
     c = S.sifar_config_default()
     c.persistent = 1
-    c.validate = S.SIFAR_VALIDATE_NONE
+    c.validate = mode
     h = ctypes.c_void_p()
     assert S.load().sifar_init(ctypes.byref(c), ctypes.byref(h)) == S.SIFAR_EINVAL
+    assert not h.value
 
 
 def test_null_handle_rejected():

@@ -340,12 +340,11 @@ def test_epilogue_residual_chain_every_node_eager():
 
 # ---- persistent decode step: producers and reduction in one launch ----------
 
-@pytest.mark.parametrize("mode", ["spec", "ordered"])
-def test_persistent_llama_decode_steps(mode):
+def test_persistent_llama_decode_steps():
     """One launch per decode step, the peers writing while the reduction runs:
     every output bit-exact; every chunk's last validation clean."""
     w = synth.LLAMA8B_DECODE
-    run = StepRun(w, 8, validate=mode, persistent=1)
+    run = StepRun(w, 8, persistent=1)
     for T in w.tokens:
         for rep in range(3):
             epochs = run.step(T)
@@ -378,8 +377,7 @@ def test_persistent_many_steps_sampled():
 
 
 @pytest.mark.parametrize("T", [4, 8])
-@pytest.mark.parametrize("order", ["spec", "ordered"])
-def test_persistent_late_stamps(order, T):
+def test_persistent_late_stamps(T):
     """Late ranks' stamps land after a delay while the reduction waits on them:
     outputs equal the oracle; the decision log shows retries and ends clean.
     T = 8 (64 chunks) runs the grouped producer: one release fence and one
@@ -387,11 +385,11 @@ def test_persistent_late_stamps(order, T):
     w = synth.SPEC_STRESS
     steps = 6
     late = synth.delay_table(w.wid, w.nranks, w.reduces_per_step * steps, w.stale_prob)
-    run = StepRun(w, T, validate=order, persistent=1, late_delay=4)
+    run = StepRun(w, T, persistent=1, late_delay=4)
     run.s.set_injection(inject_table(late))
     retried = 0
     for step in range(steps):
-        print(f"late stamps {order} T={T} step {step}", flush=True)
+        print(f"late stamps T={T} step {step}", flush=True)
         epochs = run.step(T)
         got = to_host(run.out_d)
         exp = oracle.reduce_chain(run.pool, epochs, T)
@@ -442,12 +440,16 @@ def test_persistent_epilogue_moe_chain(T):
     run.s.close()
 
 
-@pytest.mark.parametrize("N,T,H", [(5, 16, 3896), (8, 8, 4608), (3, 32, 2048)])
+@pytest.mark.parametrize("N,T,H", [(5, 16, 3896), (8, 8, 4608), (3, 32, 2048),
+                                   (8, 1, 1024), (4, 3, 1536), (2, 1, 512), (8, 5, 4608)])
 def test_persistent_ragged_shapes(N, T, H):
     """Persistent steps on shapes off the benchmark grid: 3896 leaves a partial
     last chunk inside a grouped workgroup (8 chunks per token, 128 chunks);
     4608 has 9 chunks per token, not divisible into 4-wave workgroups, so the
-    step falls back to one wave per workgroup; N = 3 with 64 chunks groups too."""
+    step falls back to one wave per workgroup; N = 3 with 64 chunks groups too.
+    The last four have a number of workgroups per plane that is not a multiple
+    of the 8 XCDs (2, 9, 1 and 45 chunks), so a chunk's producer and consumer
+    run on different XCDs and meet only through agent-scope memory."""
     w = synth.Workload(73, f"ragged-{N}-{T}-{H}", N, (T,), H, 12, 1, "normal")
     run = StepRun(w, T, persistent=1)
     for rep in range(3):
@@ -458,6 +460,26 @@ def test_persistent_ragged_shapes(N, T, H):
         for i in range(w.reduces_per_step):
             assert np.array_equal(got[i, :T], exp[i]), f"rep={rep} node={i}"
     run.s.check()
+    run.s.close()
+
+
+def test_persistent_cross_xcd_many_steps():
+    """64-all-reduce persistent steps, 2 chunks per plane (producer and
+    consumer of a chunk on different XCDs), 40 steps, sampled."""
+    w = synth.Workload(74, "cross-xcd", 8, (1,), 1024, 64, 40, "act")
+    run = StepRun(w, 1, persistent=1)
+    for step in range(w.steps):
+        epochs = run.step(1)
+        if step % 7 == 0:
+            print(f"cross-xcd step {step}", flush=True)
+            got = to_host(run.out_d)
+            for i in range(0, w.reduces_per_step, 3):
+                g = epochs[i]
+                exp = oracle.reduce(run.pool[(g - 1) % run.pool.shape[0]][:, :1])
+                assert np.array_equal(got[i, :1], exp), f"step={step} node={i}"
+    run.s.check()
+    log = run.s.read_log()[:, :2]
+    assert np.all((log >> 24) == 0)
     run.s.close()
 
 
@@ -484,8 +506,7 @@ def test_persistent_after_eager_and_graph_steps():
 
 # ---- one buffer per rank: the bottom-barrier baseline ----------------------
 
-@pytest.mark.parametrize("persistent", [0, 1])
-@pytest.mark.parametrize("mode", ["spec", "ordered"])
+@pytest.mark.parametrize("mode,persistent", [("spec", 0), ("ordered", 0), ("ordered", 1)])
 def test_single_buffer_steps(mode, persistent):
     """buffers = 1: each rank has one slot, rewritten only after the previous
     all-reduce finished reading it. Same outputs, bit-exact."""
