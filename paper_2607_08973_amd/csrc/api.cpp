@@ -160,13 +160,14 @@ int launch_red(sifar_t h, const ReduceArgs &ra, const ProduceArgs *next, hipStre
                                     h->cfg.waves_per_group, s));
 }
 
-// Waves per workgroup of a persistent step. Grouping lets one release fence
-// cover several chunks; measured on MI355X (N = 8, H = 4096) it shortens the
-// step once every XCD holds several producer waves (64 chunks: 2.66 -> 2.16 us
-// per all-reduce) and does not help below that (32 chunks: no change).
+// Waves per workgroup of a persistent step. Grouping lets one publication
+// (and, for a cross-XCD pair, one release fence) cover 4 chunks and shares a
+// CU among 4 waves. Measured on MI355X with same-XCD pairs: it lengthens the
+// step up to 256 chunks (64 chunks: 0.92 -> 1.41 us per all-reduce) and
+// shortens it from 512 on (N = 8, 1024 chunks: 4.72 -> 3.68 us).
 int chain_waves(const sifar_ctx *h, int32_t tokens) {
     const int64_t chunks = static_cast<int64_t>(tokens) * h->segs;
-    return h->chain_grouping && h->segs % kChainGroupWaves == 0 && chunks >= 64
+    return h->chain_grouping && h->segs % kChainGroupWaves == 0 && chunks >= 512
                ? kChainGroupWaves
                : 1;
 }

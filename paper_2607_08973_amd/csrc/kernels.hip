@@ -80,6 +80,16 @@ __device__ __forceinline__ void st_relaxed(uint32_t *p, uint32_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// A flag for a partner wave on this XCD: a plain store lands in the XCD's L2,
+// where the partner's agent-scope loads read it; an agent-scope store is
+// written past the L2 and becomes visible to a poller later.
+__device__ __forceinline__ void st_flag(uint32_t *p, uint32_t v, bool local) {
+    if (local)
+        __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    else
+        __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ __forceinline__ void st_release(uint32_t *p, uint32_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -274,16 +284,12 @@ __device__ __forceinline__ void load_payload(V16 (&v)[N], const uint16_t *slot0,
 // AGENT: payload through agent-scope loads (persistent chain), stamps first.
 // INJECT_HOOK: deterministic injection, the late ranks' stamps land right
 // after the first failed validation (only when producers have finished).
-// AGENT: a persistent step, whose producer may be writing right now. There
-// only ORDERED is sound: the stamps are polled with relaxed agent-scope loads,
-// and the payload is loaded once every stamp is fresh -- after an acquire
-// fence when the chunk's producer is on another XCD (`local` false), directly
-// when it shares this XCD (see publish_slot).
-template <int N, int MODE, bool AGENT, bool INJECT_HOOK>
+// Gather of a per-epoch launch: the epoch's payload was written by an earlier
+// launch, so a stale stamp can only be an injected late one.
+template <int N, int MODE, bool INJECT_HOOK>
 __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint32_t g, uint32_t p,
                                        int lane, V16 (&v)[N], uint32_t &attempts, uint32_t &first,
-                                       uint32_t &last, bool local = false) {
-    static_assert(!AGENT || MODE == kOrdered, "a persistent step validates before it loads");
+                                       uint32_t &last) {
     const Geometry &geo = a.geo;
     const uint16_t *slot0 = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + k.row;
     const uint64_t rank_step = 2 * geo.slot_elems;  // slots are [rank][parity]
@@ -291,9 +297,9 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
 
     uint32_t st = 0;
     if (MODE == kOrdered) {
-        if (k.active && lane < N) st = AGENT ? ld_relaxed(stamp + lane) : ld_acquire(stamp + lane);
+        if (k.active && lane < N) st = ld_acquire(stamp + lane);
     } else {
-        load_payload<N, AGENT>(v, slot0, rank_step);
+        load_payload<N, false>(v, slot0, rank_step);
         if (MODE == kSpec && k.active && lane < N) st = ld_relaxed(stamp + lane);
     }
 
@@ -313,18 +319,14 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
                 if (lane < N && ((inj >> lane) & 1u) && !((inj >> (8 + lane)) & 1u))
                     st_release(stamp + lane, g);
             }
-            if (AGENT && m != 0) {
-                if (latched(a.err)) break;  // the step is already failing: stop waiting
-                __builtin_amdgcn_s_sleep(1);  // a live peer is still writing
-            }
-            // Plain reloads need an acquire fence (an L2 invalidate) to see the
-            // peers' data; the persistent step polls stamps only.
-            if (!AGENT) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            // plain reloads need an acquire fence (an L2 invalidate) to see the
+            // peers' data
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             if (MODE == kOrdered) {
-                if (lane < N) st = AGENT ? ld_relaxed(stamp + lane) : ld_acquire(stamp + lane);
+                if (lane < N) st = ld_acquire(stamp + lane);
             } else {
                 if (lane < N) st = ld_relaxed(stamp + lane);
-                load_payload<N, AGENT>(v, slot0, rank_step);
+                load_payload<N, false>(v, slot0, rank_step);
             }
             ++attempts;
             m = static_cast<uint32_t>(__ballot(lane < N && st != g));
@@ -332,15 +334,48 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
             fail = m != 0 || attempts <= a.forced_retries;
         }
     }
-    if (MODE == kOrdered) {
-        if (AGENT) {
-            if (local)
-                __atomic_signal_fence(__ATOMIC_SEQ_CST);
-            else
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    if (MODE == kOrdered) load_payload<N, false>(v, slot0, rank_step);
+}
+
+// Persistent-step gather of an active chunk: a producer may be writing right
+// now, so only ORDERED is sound. `st` holds this lane's first stamp poll
+// (issued by the caller); polls repeat (relaxed agent-scope loads, short
+// sleeps) until every stamp is fresh, then the payload is loaded -- after an
+// acquire fence when the producer is on another XCD, directly when it shares
+// this XCD (see publish_slot).
+template <int N>
+__device__ __forceinline__ void gather_chain(const ReduceArgs &a, const Chunk &k, uint32_t g,
+                                             uint32_t p, int lane, uint32_t st, V16 (&v)[N],
+                                             uint32_t &attempts, uint32_t &first,
+                                             uint32_t &last, bool local) {
+    const Geometry &geo = a.geo;
+    const uint16_t *slot0 = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + k.row;
+    const uint64_t rank_step = 2 * geo.slot_elems;  // slots are [rank][parity]
+    const uint32_t *stamp = a.stamps + (static_cast<size_t>(p) * geo.w_max + k.c) * N;
+    attempts = 1;
+    uint32_t m = static_cast<uint32_t>(__ballot(lane < N && st != g));
+    first = last = m;
+    bool fail = m != 0 || a.forced_retries >= 1;
+    while (fail) {
+        if (attempts >= a.max_attempts) {
+            if (lane == 0) latch(a.err, kErrRetryBudget, g, k.c, attempts);
+            break;
         }
-        load_payload<N, AGENT>(v, slot0, rank_step);
+        if (m != 0) {
+            if (latched(a.err)) break;  // the step is already failing: stop waiting
+            __builtin_amdgcn_s_sleep(1);
+        }
+        if (lane < N) st = ld_relaxed(stamp + lane);
+        ++attempts;
+        m = static_cast<uint32_t>(__ballot(lane < N && st != g));
+        last = m;
+        fail = m != 0 || attempts <= a.forced_retries;
     }
+    if (local)
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    else
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    load_payload<N, true>(v, slot0, rank_step);
 }
 
 // Fixed-order fp32 sum: acc = x_0; acc += x_1; ... acc += x_{N-1}; then bf16.
@@ -477,7 +512,7 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
     const uint32_t g = epoch_of(a.ep);
     V16 v[N];
     uint32_t attempts, first, last;
-    gather<N, MODE, false, true>(a, k, g, p, lane, v, attempts, first, last);
+    gather<N, MODE, true>(a, k, g, p, lane, v, attempts, first, last);
     const V16 o = sum_round<N>(v);
     if (k.active && lane == 0) {
         write_log(a, k, g, log_word(attempts, first, last));
@@ -544,13 +579,13 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
         const uint32_t held = held_back(a.inject, a.inject_entries, g);
         publish_slot(local);
         uint32_t *stamp = a.stamps + pc * N;
-        if (lane < N && !((held >> lane) & 1u)) st_relaxed(stamp + lane, g);
-        if (lane == 0) st_relaxed(a.produced + pc, g);
+        if (lane < N && !((held >> lane) & 1u)) st_flag(stamp + lane, g, local);
+        if (lane == 0) st_flag(a.produced + pc, g, local);
         if (held) {
             const uint32_t inj = a.inject[(g - 1u) % static_cast<uint32_t>(a.inject_entries)];
             for (uint32_t d = 0; d < A.late_delay; ++d) __builtin_amdgcn_s_sleep(8);
             if (lane < N && ((inj >> lane) & 1u) && !((inj >> (8 + lane)) & 1u))
-                st_relaxed(stamp + lane, g);
+                st_flag(stamp + lane, g, local);
         }
     }
 }
@@ -595,7 +630,7 @@ __device__ __forceinline__ void chain_producer_grouped(const ChainArgs &A, uint3
                 // here, not after wave 0's fence, keeps the next epoch's slot
                 // check from seeing the previous value (with one buffer that
                 // would let the slot be rewritten before it is consumed)
-                if (lane == 0) st_relaxed(a.produced + pc, g);
+                if (lane == 0) st_flag(a.produced + pc, g, true);
             }
         }
         __builtin_amdgcn_s_waitcnt(0);  // this wave's slot stores have reached L2
@@ -605,12 +640,12 @@ __device__ __forceinline__ void chain_producer_grouped(const ChainArgs &A, uint3
             publish_slot(local);  // with `local` the wait above already did it
             const size_t ps = static_cast<size_t>(p) * geo.w_max + ks.c;
             uint32_t *stamp = a.stamps + ps * N;
-            if (stamper && !((held >> sr) & 1u)) st_relaxed(stamp + sr, g);
+            if (stamper && !((held >> sr) & 1u)) st_flag(stamp + sr, g, local);
             if (held) {
                 const uint32_t inj = a.inject[(g - 1u) % static_cast<uint32_t>(a.inject_entries)];
                 for (uint32_t d = 0; d < A.late_delay; ++d) __builtin_amdgcn_s_sleep(8);
                 if (stamper && ((inj >> sr) & 1u) && !((inj >> (8 + sr)) & 1u))
-                    st_relaxed(stamp + sr, g);
+                    st_flag(stamp + sr, g, local);
             }
         }
     }
@@ -628,19 +663,25 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
     const bool local = k.active && partner_is_local(A.place + geo.w_max + k.c, base, lane);
     V16 wv;
     if (EPI) wv = ld16(a.weight + k.elem);
+    const uint32_t *stamps = a.stamps + static_cast<size_t>(k.c) * N + lane;
+    const size_t parity_stride = static_cast<size_t>(geo.w_max) * N;
     for (int i = 0; i < A.reduces; ++i) {
         const uint32_t g = base + static_cast<uint32_t>(i) + 1u;
         const uint32_t p = static_cast<uint32_t>(i + 1) & A.parity_mask;
+        // read now, acted on after the payload: waiting for the payload covers it
+        const uint32_t err_seen = ld_relaxed(a.err);
         V16 rv;
         if (EPI) rv = ld16(a.residual + k.row);  // this wave's own previous store
         V16 v[N];
         uint32_t attempts, first, last;
-        gather<N, MODE, true, false>(a, k, g, p, lane, v, attempts, first, last, local);
+        uint32_t st = 0;
+        if (lane < N) st = ld_relaxed(stamps + p * parity_stride);
+        gather_chain<N>(a, k, g, p, lane, st, v, attempts, first, last, local);
         const V16 o = sum_round<N>(v);
         complete(o);  // every payload load has returned before the slot is released
         if (lane == 0) {
             write_log(a, k, g, log_word(attempts, first, last));
-            st_relaxed(a.consumed + static_cast<size_t>(p) * geo.w_max + k.c, g);
+            st_flag(a.consumed + static_cast<size_t>(p) * geo.w_max + k.c, g, local);
         }
         const uint64_t ring = static_cast<uint64_t>(i) * A.ring_stride;
         if (!EPI) {
@@ -650,8 +691,8 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
         }
         // a bounded wait failed somewhere: stop the step
         if (GROUPED && EPI) {
-            if (__syncthreads_or(latched(a.err))) return;
-        } else if (latched(a.err)) {
+            if (__syncthreads_or(err_seen != 0)) return;
+        } else if (err_seen != 0) {
             return;
         }
     }
