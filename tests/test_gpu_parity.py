@@ -483,6 +483,30 @@ def test_persistent_cross_xcd_many_steps():
     run.s.close()
 
 
+@pytest.mark.parametrize("N,T,H", [(8, 5, 4608), (8, 1, 1024)])
+def test_persistent_cross_xcd_every_output(N, T, H):
+    """150 persistent steps of 12 all-reduces with each chunk's producer and
+    consumer on different XCDs, every output checked. A reduction that loaded
+    the payload together with the stamps (the paper's speculation) accepted a
+    rank's previous epoch under a fresh stamp in ~2 % of these all-reduces;
+    the persistent step must validate before it loads."""
+    w = synth.Workload(75, f"cross-xcd-{N}-{T}-{H}", N, (T,), H, 12, 150, "normal")
+    run = StepRun(w, T, persistent=1)
+    P = run.pool.shape[0]
+    bad = []
+    for step in range(w.steps):
+        if step % 50 == 0:
+            print(f"cross-xcd every output N={N} T={T} H={H} step {step}", flush=True)
+        epochs = run.step(T)
+        got = to_host(run.out_d)
+        for i, g in enumerate(epochs):
+            if not np.array_equal(got[i, :T], oracle.reduce(run.pool[(g - 1) % P][:, :T])):
+                bad.append((step, i))
+    run.s.check()
+    run.s.close()
+    assert not bad, f"{len(bad)} of {w.steps * w.reduces_per_step} all-reduces differ: {bad[:5]}"
+
+
 def test_persistent_after_eager_and_graph_steps():
     """Eager epochs, fused graph steps and persistent steps on one handle."""
     w = synth.Workload(71, "mixed-modes", 8, (2,), 4096, 6, 1, "act")
