@@ -190,6 +190,23 @@ def cpu_baseline(pool, tokens, budget_s):
     return mean_us, per_t
 
 
+def host_cpu() -> str:
+    """Model name of the host CPU and the cores this process may use."""
+    model = "unknown CPU"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        avail = os.cpu_count() or 0
+    return f"{model}, {avail} cores available"
+
+
 def time_steps(s, T, steps, stream):
     """HIP-event time of `steps` replays of the step graph for T tokens (ms)."""
     import torch
@@ -577,9 +594,9 @@ def main():
         cpu_us, cpu_t = cpu_baseline(pool, tokens, args.cpu_seconds)
         cpu = {"value": round(cpu_us, 3), "unit": "us per all-reduce", "cores": 1,
                "kind": "oracle",
-               "sample": f"C oracle, 1 thread, the same N=8 x H=4096 pool entries at batch "
-                         f"{list(tokens)} for {args.cpu_seconds:.0f} s total; mean over batch sizes "
-                         f"of per-reduce time: " +
+               "sample": f"C oracle, 1 thread ({host_cpu()}), the same N=8 x H=4096 pool "
+                         f"entries at batch {list(tokens)} for {args.cpu_seconds:.0f} s total; mean "
+                         f"over batch sizes of per-reduce time: " +
                          ", ".join(f"T={t}: {v:.1f} us" for t, v in cpu_t.items())}
 
     s.close()
