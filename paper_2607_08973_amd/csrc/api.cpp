@@ -314,15 +314,20 @@ int sifar_init(const sifar_config *cfg, sifar_t *out) {
     h->exch_q = c.persistent && h->segs > h->groups_per_token ? h->segs : h->groups_per_token;
     if (c.persistent) {
         // every consumer and producer wave of a step is resident at once
+        // with the epilogue the grid pads the tokens to a multiple of 8 (one
+        // XCD per token)
+        const int64_t tokens = c.epilogue ? 8 * ((static_cast<int64_t>(c.max_tokens) + 7) / 8)
+                                          : c.max_tokens;
+        const int64_t waves = 2 * tokens * h->segs;
         const int cap = max_active_chain_groups(c.nranks, c.validate, c.epilogue != 0, 1);
-        if (cap <= 0 || 2 * static_cast<int64_t>(h->w_max) > cap) {
+        if (cap <= 0 || waves > cap) {
             delete h;
             return SIFAR_EINVAL;
         }
         const int gcap = max_active_chain_groups(c.nranks, c.validate, c.epilogue != 0,
                                                  kChainGroupWaves);
         h->chain_grouping = c.nranks * kChainGroupWaves <= kLanes && gcap > 0 &&
-                            2 * static_cast<int64_t>(h->w_max) / kChainGroupWaves <= gcap;
+                            waves / kChainGroupWaves <= gcap;
     }
     rc = SIFAR_OK;
     if (!rc) rc = dev_alloc(&h->slots, static_cast<size_t>(c.nranks) * 2 * h->slot_elems);

@@ -208,6 +208,18 @@ __device__ __forceinline__ bool partner_is_local(const uint64_t *place, uint32_t
     return __builtin_amdgcn_readfirstlane(local) != 0;
 }
 
+// Per lane: does the wave whose tag is *place run on this XCD? (bounded wait)
+__device__ __forceinline__ bool tag_is_local(const uint64_t *place, uint32_t base) {
+    const uint64_t want = place_tag(base, xcc_id());
+    uint64_t t = 0;
+    for (uint32_t spins = 0; spins < kPlaceSpins; ++spins) {
+        t = __hip_atomic_load(place, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((t >> 32) == (want >> 32)) break;
+        __builtin_amdgcn_s_sleep(1);
+    }
+    return t == want;
+}
+
 // Publication of a producer's slot stores before its stamps. To a consumer on
 // another XCD: an agent-scope release fence, which writes back this XCD's L2.
 // To a consumer on this XCD: waiting until the stores have reached the L2 is
@@ -414,7 +426,7 @@ __device__ __forceinline__ void write_log(const ReduceArgs &a, const Chunk &k, u
 __device__ __forceinline__ void residual_rmsnorm(const ReduceArgs &a, const Chunk &k, uint32_t g,
                                                  const V16 &o, const V16 &rv,
                                                  const V16 &wv, uint16_t *y, int lane, int wave,
-                                                 int G, int q) {
+                                                 int G, int q, bool xlocal = false) {
     const Geometry &geo = a.geo;
     // res' = bf16(a + res), with a = the bf16 all-reduce result.
     V16 nr;
@@ -451,7 +463,11 @@ __device__ __forceinline__ void residual_rmsnorm(const ReduceArgs &a, const Chun
                            static_cast<size_t>(k.t) * Q;
             if (lane == 0) {
                 const uint64_t word = (static_cast<uint64_t>(g) << 32) | __float_as_uint(grp);
-                __hip_atomic_store(ex + q, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                // all groups of the token on this XCD: the word meets them in its L2
+                if (xlocal)
+                    __hip_atomic_store(ex + q, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                else
+                    __hip_atomic_store(ex + q, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
             uint64_t mine = 0;
             uint32_t spins = 0;
@@ -554,10 +570,11 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
 // several chunks per wave behind one fence does not shorten the step -- the
 // dual-buffer rule ties the producer of g + 1 to the reduction of g - 1.)
 template <int N, int MODE, bool EPI>
-__device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base, int lane) {
+__device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base, int lane,
+                                               int bx, int by) {
     const ProduceArgs &a = A.p;
     const Geometry &geo = a.geo;
-    const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x, lane);
+    const Chunk k = chunk_at(geo, by, bx, lane);
     publish_place(A.place + geo.w_max + k.c, base, lane);
     const bool local = partner_is_local(A.place + k.c, base, lane);
     for (int i = 0; i < A.reduces; ++i) {
@@ -601,12 +618,12 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
 // workgroup at the same barrier.
 template <int N>
 __device__ __forceinline__ void chain_producer_grouped(const ChainArgs &A, uint32_t base,
-                                                       int lane, int wave, int G) {
+                                                       int lane, int wave, int G, int bx, int by) {
     const ProduceArgs &a = A.p;
     const Geometry &geo = a.geo;
-    const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x * G + wave, lane);
+    const Chunk k = chunk_at(geo, by, bx * G + wave, lane);
     const int sw = lane / N, sr = lane - sw * N;
-    const Chunk ks = chunk_at(geo, blockIdx.y, blockIdx.x * G + (sw < G ? sw : 0), 0);
+    const Chunk ks = chunk_at(geo, by, bx * G + (sw < G ? sw : 0), 0);
     const bool stamper = wave == 0 && sw < G && ks.active;
     if (k.active) publish_place(A.place + geo.w_max + k.c, base, lane);
     const bool mine = !k.active || partner_is_local(A.place + k.c, base, lane);
@@ -655,12 +672,20 @@ __device__ __forceinline__ void chain_producer_grouped(const ChainArgs &A, uint3
 // group's waves share the RMSNorm barriers, so they also leave together.
 template <int N, int MODE, bool EPI, bool GROUPED>
 __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base, int lane,
-                                               int wave, int G) {
+                                               int wave, int G, int bx, int by) {
     const ReduceArgs &a = A.r;
     const Geometry &geo = a.geo;
-    const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x * G + wave, lane);
+    const Chunk k = chunk_at(geo, by, bx * G + wave, lane);
     if (k.active) publish_place(A.place + k.c, base, lane);
     const bool local = k.active && partner_is_local(A.place + geo.w_max + k.c, base, lane);
+    // the epilogue's exchange partners: wave 0 of each group of this token
+    bool xlocal = false;
+    if (EPI && wave == 0) {
+        const int Q = a.groups_per_token;
+        const bool mine = lane >= Q ||
+                          tag_is_local(A.place + static_cast<size_t>(k.t) * geo.segs + lane * G, base);
+        xlocal = __ballot(!mine) == 0;
+    }
     V16 wv;
     if (EPI) wv = ld16(a.weight + k.elem);
     const uint32_t *stamps = a.stamps + static_cast<size_t>(k.c) * N + lane;
@@ -687,7 +712,7 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
         if (!EPI) {
             if (k.lane_ok) st16(a.out + ring + k.row, o);
         } else {
-            residual_rmsnorm(a, k, g, o, rv, wv, a.y + ring, lane, wave, G, blockIdx.x);
+            residual_rmsnorm(a, k, g, o, rv, wv, a.y + ring, lane, wave, G, bx, xlocal);
         }
         // a bounded wait failed somewhere: stop the step
         if (GROUPED && EPI) {
@@ -710,13 +735,28 @@ __global__ __launch_bounds__(GROUPED ? kChainGroupWaves * kLanes : kLanes) void 
     const int wave = GROUPED ? static_cast<int>(threadIdx.x) / kLanes : 0;
     const int G = GROUPED ? static_cast<int>(blockDim.x) / kLanes : 1;
     const uint32_t base = A.r.ep.base[0];
-    if (blockIdx.z == 1) {
-        if (GROUPED)
-            chain_producer_grouped<N>(A, base, lane, wave, G);
-        else
-            chain_producer<N, MODE, EPI>(A, base, lane);
-    } else {
-        chain_consumer<N, MODE, EPI, GROUPED>(A, base, lane, wave, G);
+    // Logical (group, token). With the epilogue, workgroup b of a plane serves
+    // token (b mod 8) + 8 * (b / 8 / Q), group (b / 8) mod Q: every group of a
+    // token -- consumers and producers, since each plane holds a multiple of 8
+    // workgroups -- is dealt to the same XCD, so the per-epoch exchange of the
+    // token's sum of squares stays in one L2. Workgroups past the last token
+    // only arrive on the counter.
+    int bx = blockIdx.x, by = blockIdx.y;
+    if (EPI) {
+        const int Q = A.r.groups_per_token;
+        const int j = static_cast<int>(blockIdx.x) >> 3;
+        bx = j % Q;
+        by = (static_cast<int>(blockIdx.x) & 7) + 8 * (j / Q);
+    }
+    if (by < A.r.geo.tokens) {
+        if (blockIdx.z == 1) {
+            if (GROUPED)
+                chain_producer_grouped<N>(A, base, lane, wave, G, bx, by);
+            else
+                chain_producer<N, MODE, EPI>(A, base, lane, bx, by);
+        } else {
+            chain_consumer<N, MODE, EPI, GROUPED>(A, base, lane, wave, G, bx, by);
+        }
     }
     if (lane == 0) {
         const uint32_t waves = 2u * gridDim.x * gridDim.y * static_cast<uint32_t>(G);
@@ -891,8 +931,11 @@ hipError_t launch_chain(const ChainArgs &a, int mode, bool epilogue, int waves, 
     if (a.r.geo.segs != a.p.geo.segs || a.r.geo.tokens != a.p.geo.tokens ||
         a.r.geo.segs % waves != 0 || (waves > 1 && waves * a.r.geo.nranks > kLanes))
         return hipErrorInvalidValue;
-    const dim3 grid(static_cast<uint32_t>(a.r.geo.segs / waves),
-                    static_cast<uint32_t>(a.r.geo.tokens), 2);
+    const uint32_t q = static_cast<uint32_t>(a.r.geo.segs / waves);
+    const uint32_t t8 = (static_cast<uint32_t>(a.r.geo.tokens) + 7u) / 8u;
+    if (epilogue && a.r.groups_per_token != static_cast<int32_t>(q)) return hipErrorInvalidValue;
+    const dim3 grid = epilogue ? dim3(8u * t8 * q, 1, 2)
+                               : dim3(q, static_cast<uint32_t>(a.r.geo.tokens), 2);
     void *args[] = {const_cast<ChainArgs *>(&a)};
     return hipLaunchKernel(fn, grid, dim3(kLanes * waves), args, 0, s);
 }
