@@ -702,12 +702,21 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
         uint32_t st = 0;
         if (lane < N) st = ld_relaxed(stamps + p * parity_stride);
         gather_chain<N>(a, k, g, p, lane, st, v, attempts, first, last, local);
-        const V16 o = sum_round<N>(v);
-        complete(o);  // every payload load has returned before the slot is released
-        if (lane == 0) {
-            write_log(a, k, g, log_word(attempts, first, last));
-            st_flag(a.consumed + static_cast<size_t>(p) * geo.w_max + k.c, g, local);
+        uint32_t *consumed = a.consumed + static_cast<size_t>(p) * geo.w_max + k.c;
+        if (!EPI) {
+            // release the slot as soon as every payload load has returned (the
+            // sum works on registers); measured faster for the plain chain,
+            // slower with the epilogue
+#pragma unroll
+            for (int r = 0; r < N; ++r) complete(v[r]);
+            if (lane == 0) st_flag(consumed, g, local);
         }
+        const V16 o = sum_round<N>(v);
+        if (EPI) {
+            complete(o);  // every payload load has returned before the slot is released
+            if (lane == 0) st_flag(consumed, g, local);
+        }
+        if (lane == 0) write_log(a, k, g, log_word(attempts, first, last));
         const uint64_t ring = static_cast<uint64_t>(i) * A.ring_stride;
         if (!EPI) {
             if (k.lane_ok) st16(a.out + ring + k.row, o);
