@@ -222,7 +222,11 @@ int sifar_bind_step(sifar_t h, const sifar_step_buffers *b);
  * The graph for a token count is captured on first use (on a library-owned
  * stream) and replayed afterwards; epochs and parities come from a
  * device-resident counter, so a replay needs no host work. Requires no
- * produced-but-unreduced epoch (SIFAR_ESTATE). */
+ * produced-but-unreduced epoch (SIFAR_ESTATE).
+ * A persistent step needs all its waves resident at once (checked at init
+ * against an otherwise idle GPU); persistent steps of several handles that run
+ * concurrently on different streams may not fit together, and then end with a
+ * latched SIFAR_EDEVICE (every wait is bounded) instead of completing. */
 int sifar_step(sifar_t h, int32_t tokens, void *stream);
 
 /* ---- injection, logs, state --------------------------------------------------- */
@@ -241,7 +245,9 @@ int sifar_log_geometry(sifar_t h, int32_t *log_epochs, int32_t *chunks_per_token
 
 /* Copy the decision log to host memory (synchronises the device). Each word:
  * bits 0-15 attempts (saturating), 16-23 stale-rank mask of the first
- * validation, 24-31 stale-rank mask of the last one. `words` must be at most
+ * validation, 24-31 stale-rank mask of the last one. An attempt is one
+ * validation: in per-epoch launches a load of stamps and payload, in a
+ * persistent step one poll of the stamps. `words` must be at most
  * log_epochs * w_max. */
 int sifar_read_log(sifar_t h, uint32_t *host_dst, size_t words);
 
