@@ -115,22 +115,31 @@ TRAFFIC_PROFILES = {
 }
 
 
+def kernel_code_digest() -> str:
+    """sha256 of kernels.hip with comments, trailing blanks and empty lines
+    removed: it changes when the kernel code does, not when a comment does."""
+    import hashlib
+    import re
+
+    src = open(os.path.join(ROOT, "paper_2607_08973_amd", "csrc", "kernels.hip")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    lines = [re.sub(r"//.*$", "", ln).rstrip() for ln in src.splitlines()]
+    code = "\n".join(ln for ln in lines if ln)
+    return hashlib.sha256(code.encode()).hexdigest()
+
+
 def measured_traffic(kind):
     """HBM bytes per launch of the dominant kernel from the committed FETCH_SIZE /
-    WRITE_SIZE profile, or None when the kernel source changed since."""
-    import hashlib
-
+    WRITE_SIZE profile, or None when the kernel code changed since."""
     path = TRAFFIC_PROFILES[kind]
     if not os.path.exists(path):
         return None
     kv = {}
     for line in open(path):
-        if ":" in line and line.split(":")[0] in ("traffic_bytes_per_launch", "kernels_hip_sha256"):
+        if ":" in line and line.split(":")[0] in ("traffic_bytes_per_launch", "kernel_code_digest"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    src = os.path.join(ROOT, "paper_2607_08973_amd", "csrc", "kernels.hip")
-    cur = hashlib.sha256(open(src, "rb").read()).hexdigest()
-    if kv.get("kernels_hip_sha256") != cur or "traffic_bytes_per_launch" not in kv:
+    if kv.get("kernel_code_digest") != kernel_code_digest() or "traffic_bytes_per_launch" not in kv:
         return None
     return float(kv["traffic_bytes_per_launch"])
 

@@ -8,22 +8,27 @@
 //
 // Two ways to run a decode step:
 //  - per-epoch launches (eager calls, step graphs): the producer of an epoch
-//    always finishes in an earlier launch than the reduction of that epoch;
+//    always finishes in an earlier launch than the reduction of that epoch, so
+//    the paper's speculative reduction (SPEC) is exact here;
 //  - one persistent launch per step (chain_kernel): consumer and producer
 //    waves run concurrently and synchronise through stamps and per-chunk
-//    consumed/produced words, with agent-scope release/acquire.
+//    consumed/produced words; the consumer validates before it loads
+//    (ORDERED), since speculative loads racing a live producer were measured
+//    to accept stale data.
 //
 // Memory-model choices (LLVM AMDGPU memory model for GFX942/950; the 8 XCDs
 // have separate L2s, so agent scope means "coherent across XCDs"):
 //  - stamps are read with agent-scope atomic loads;
-//  - SPEC issues the payload loads and the stamp loads together, with no
-//    ordering between them (the paper's concurrent payload warps and
-//    validation warp); ORDERED acquires the stamps before loading the payload;
-//  - a retry starts with an acquire fence so the reloads cannot be served
-//    from a stale cache line (the paper's L1-bypassing re-read, Sec. 4.2);
-//  - in the persistent chain the payload is read with agent-scope loads too
-//    (no stale L2 line from the slot's previous use), and the producer
-//    publishes with one agent-scope release fence per wave and epoch.
+//  - per-epoch SPEC issues the payload loads and the stamp loads together (the
+//    paper's concurrent payload warps and validation warp); ORDERED acquires
+//    the stamps before loading the payload; a retry starts with an acquire
+//    fence so the reloads cannot be served from a stale cache line (the
+//    paper's L1-bypassing re-read, Sec. 4.2);
+//  - in the persistent chain each wave learns whether its partner shares its
+//    XCD. Same-XCD pairs meet in that XCD's L2: plain flag stores, a wait for
+//    the slot stores instead of a release fence, agent-scope (L1-bypassing)
+//    loads. Cross-XCD pairs use agent-scope stores, a release fence before the
+//    stamps and an acquire fence before the payload loads.
 //
 // Arithmetic: fp32 adds in ascending rank order (no reassociation, no FMA
 // contraction), bf16 rounding by the native V_CVT_PK_BF16_F32 (round to nearest
@@ -292,12 +297,11 @@ __device__ __forceinline__ void load_payload(V16 (&v)[N], const uint16_t *slot0,
                                              : ld16(slot0 + r * rank_step);
 }
 
-// Load chunk k of epoch g, validate its N stamps, retry while any is stale.
-// AGENT: payload through agent-scope loads (persistent chain), stamps first.
+// Gather of a per-epoch launch: load chunk k of epoch g, validate its N
+// stamps, retry while any is stale. The epoch's payload was written by an
+// earlier launch, so a stale stamp can only be an injected late one.
 // INJECT_HOOK: deterministic injection, the late ranks' stamps land right
-// after the first failed validation (only when producers have finished).
-// Gather of a per-epoch launch: the epoch's payload was written by an earlier
-// launch, so a stale stamp can only be an injected late one.
+// after the first failed validation.
 template <int N, int MODE, bool INJECT_HOOK>
 __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint32_t g, uint32_t p,
                                        int lane, V16 (&v)[N], uint32_t &attempts, uint32_t &first,
@@ -569,7 +573,7 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
 // (Measured on MI355X: prefetching the next epoch's sources or batching
 // several chunks per wave behind one fence does not shorten the step -- the
 // dual-buffer rule ties the producer of g + 1 to the reduction of g - 1.)
-template <int N, int MODE, bool EPI>
+template <int N>
 __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base, int lane,
                                                int bx, int by) {
     const ProduceArgs &a = A.p;
@@ -762,7 +766,7 @@ __global__ __launch_bounds__(GROUPED ? kChainGroupWaves * kLanes : kLanes) void 
             if (GROUPED)
                 chain_producer_grouped<N>(A, base, lane, wave, G, bx, by);
             else
-                chain_producer<N, MODE, EPI>(A, base, lane, bx, by);
+                chain_producer<N>(A, base, lane, bx, by);
         } else {
             chain_consumer<N, MODE, EPI, GROUPED>(A, base, lane, wave, G, bx, by);
         }
