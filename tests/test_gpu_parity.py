@@ -441,15 +441,17 @@ def test_persistent_epilogue_moe_chain(T):
 
 
 @pytest.mark.parametrize("N,T,H", [(5, 16, 3896), (8, 8, 4608), (3, 32, 2048),
-                                   (8, 1, 1024), (4, 3, 1536), (2, 1, 512), (8, 5, 4608)])
+                                   (8, 1, 1024), (4, 3, 1536), (2, 1, 512), (8, 5, 4608),
+                                   (1, 4, 2048), (7, 2, 4096), (6, 128, 4096)])
 def test_persistent_ragged_shapes(N, T, H):
     """Persistent steps on shapes off the benchmark grid: 3896 leaves a partial
     last chunk inside a grouped workgroup (8 chunks per token, 128 chunks);
     4608 has 9 chunks per token, not divisible into 4-wave workgroups, so the
     step falls back to one wave per workgroup; N = 3 with 64 chunks groups too.
-    The last four have a number of workgroups per plane that is not a multiple
+    The next four have a number of workgroups per plane that is not a multiple
     of the 8 XCDs (2, 9, 1 and 45 chunks), so a chunk's producer and consumer
-    run on different XCDs and meet only through agent-scope memory."""
+    run on different XCDs and meet only through agent-scope memory. Then one
+    rank, an odd rank count, and 1024 chunks in 4-wave workgroups at N = 6."""
     w = synth.Workload(73, f"ragged-{N}-{T}-{H}", N, (T,), H, 12, 1, "normal")
     run = StepRun(w, T, persistent=1)
     for rep in range(3):
