@@ -211,18 +211,20 @@ typedef struct {
 int sifar_bind_step(sifar_t h, const sifar_step_buffers *b);
 
 /* Enqueue one decode step for `tokens` tokens: L all-reduces plus one
- * epoch-counter advance, as one hipGraphLaunch. With fuse_peers the graph is
- * produce(g1), then L-1 launches that each reduce g_i while writing g_(i+1),
- * then reduce(g_L): L + 1 kernel nodes; without it, L x (produce, reduce);
- * with persistent, one launch for the whole step. In a persistent step the
+ * epoch-counter advance. Per-epoch steps are one hipGraphLaunch: with
+ * fuse_peers the graph is produce(g1), then L-1 launches that each reduce g_i
+ * while writing g_(i+1), then reduce(g_L): L + 1 kernel nodes; without it,
+ * L x (produce, reduce). A persistent step is one kernel launch for the whole
+ * step (a one-node graph replay measured slower). In a persistent step the
  * peers run concurrently with the reduction, so a reduction often reaches an
  * epoch before its stamps (the decision log records the polls: attempts and
  * the stale ranks of the first and last poll), and injected late stamps land
  * after late_delay instead of after the first failed validation.
- * The graph for a token count is captured on first use (on a library-owned
- * stream) and replayed afterwards; epochs and parities come from a
- * device-resident counter, so a replay needs no host work. Requires no
- * produced-but-unreduced epoch (SIFAR_ESTATE).
+ * A per-epoch step's graph for a token count is captured on first use (on a
+ * library-owned stream) and replayed afterwards; epochs and parities come
+ * from a device-resident counter, so neither a replay nor a persistent
+ * launch needs per-all-reduce host work. Requires no produced-but-unreduced
+ * epoch (SIFAR_ESTATE).
  * A persistent step needs all its waves resident at once (checked at init
  * against an otherwise idle GPU); persistent steps of several handles that run
  * concurrently on different streams may not fit together, and then end with a
