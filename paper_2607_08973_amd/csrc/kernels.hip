@@ -737,7 +737,8 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
 }
 
 // Grid (segs / G, tokens, 2) of G-wave workgroups (G = 1, or kChainGroupWaves
-// when GROUPED): plane 0 reduces chunk (t, x * G + wave) for epochs
+// when GROUPED), or (8 * ceil(tokens / 8) * Q, 1, 2) with the epilogue (Q =
+// segs / G, layout below): plane 0 reduces chunk (t, x * G + wave) for epochs
 // base+1 .. base+L in order, plane 1 produces it. The last wave to arrive on
 // the counter advances the epoch base for the next step: every wave read the
 // base before it arrived, so no wave can see the advanced value.
