@@ -201,6 +201,7 @@ int chain_args(const sifar_t h, int32_t tokens, ChainArgs *ca) {
     return waves;
 }
 
+// Graph of a per-epoch step (persistent steps are one direct launch).
 int capture_step(sifar_t h, int32_t tokens, hipGraphExec_t *out) {
     const int L = h->cfg.reduces_per_step;
     const uint32_t advance = static_cast<uint32_t>(L + (L & 1));
@@ -224,11 +225,7 @@ int capture_step(sifar_t h, int32_t tokens, hipGraphExec_t *out) {
     };
     ProduceArgs pa{}, pn{};
     ReduceArgs ra{}, rn{};
-    if (h->cfg.persistent) {
-        ChainArgs ca{};
-        const int waves = chain_args(h, tokens, &ca);
-        rc = hip_status(launch_chain(ca, h->cfg.validate, h->cfg.epilogue != 0, waves, s));
-    } else if (h->cfg.fuse_peers && h->cfg.buffers == 2) {
+    if (h->cfg.fuse_peers && h->cfg.buffers == 2) {
         node_args(0, &pa, &ra);
         rc = hip_status(launch_produce(pa, h->cfg.waves_per_group, s));
         for (int i = 0; i < L && rc == SIFAR_OK; ++i) {
@@ -247,8 +244,7 @@ int capture_step(sifar_t h, int32_t tokens, hipGraphExec_t *out) {
             if (rc == SIFAR_OK) rc = launch_red(h, ra, nullptr, s);
         }
     }
-    if (rc == SIFAR_OK && !h->cfg.persistent)  // the persistent launch advances it itself
-        rc = hip_status(launch_advance(&h->state->epoch_base, advance, s));
+    if (rc == SIFAR_OK) rc = hip_status(launch_advance(&h->state->epoch_base, advance, s));
     hipGraph_t graph = nullptr;
     const hipError_t e = hipStreamEndCapture(s, &graph);
     if (rc == SIFAR_OK && e != hipSuccess) rc = SIFAR_EHIP;
