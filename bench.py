@@ -115,17 +115,23 @@ TRAFFIC_PROFILES = {
 }
 
 
+KERNEL_SOURCES = ("kernels.hip", "coherence.h", "sifar_kernels.h")
+
+
 def kernel_code_digest() -> str:
-    """sha256 of kernels.hip with comments, trailing blanks and empty lines
-    removed: it changes when the kernel code does, not when a comment does."""
+    """sha256 of the kernel sources (kernels.hip and the headers it includes
+    from csrc/) with comments, trailing blanks and empty lines removed: it
+    changes when the kernel code does, not when a comment does."""
     import hashlib
     import re
 
-    src = open(os.path.join(ROOT, "paper_2607_08973_amd", "csrc", "kernels.hip")).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    lines = [re.sub(r"//.*$", "", ln).rstrip() for ln in src.splitlines()]
-    code = "\n".join(ln for ln in lines if ln)
-    return hashlib.sha256(code.encode()).hexdigest()
+    code = []
+    for name in KERNEL_SOURCES:
+        src = open(os.path.join(ROOT, "paper_2607_08973_amd", "csrc", name)).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        lines = [re.sub(r"//.*$", "", ln).rstrip() for ln in src.splitlines()]
+        code.append("\n".join(ln for ln in lines if ln))
+    return hashlib.sha256("\n".join(code).encode()).hexdigest()
 
 
 def measured_traffic(kind):
@@ -162,7 +168,7 @@ def parse():
     ap.add_argument("--floor-nodes", type=int, default=64)
     ap.add_argument("--workload", default="llama8b-decode",
                     choices=["llama8b-decode", "smoke-n2", "spec-stress", "sweep", "moe-rmsnorm",
-                             "ablation", "retry-curve", "reduce-cold"],
+                             "ablation", "retry-curve", "reduce-cold", "litmus"],
                     help="llama8b-decode is the headline line; the others print one "
                          "JSON line per configuration")
     ap.add_argument("--wpg", type=int, default=1, choices=[1, 2, 4, 8, 16],
@@ -170,7 +176,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline (0 disables it)")
     args = ap.parse_args()
-    steps_persistent = args.persistent and args.workload not in ("ablation", "reduce-cold")
+    steps_persistent = args.persistent and args.workload not in ("ablation", "reduce-cold",
+                                                                 "litmus")
     if args.mode is None:
         args.mode = "ordered" if steps_persistent else "spec"
     if steps_persistent and args.mode != "ordered":
@@ -411,6 +418,26 @@ def suite(args):
         for p in pts:
             print(json.dumps({k: (round(v, 4) if isinstance(v, float) else v)
                               for k, v in p.items()}), flush=True)
+        return
+    if args.workload == "litmus":
+        # the handoff litmus (sifar_litmus): both reader orders, producer and
+        # consumer on different XCDs or on one, 8 to 512 concurrent pairs
+        import paper_2607_08973_amd as S
+        trials = 65536
+        for proto, pname in ((S.SIFAR_LITMUS_ORDERED, "ordered"),
+                             (S.SIFAR_LITMUS_READ_FIRST, "read-first")):
+            for place, lname in ((S.SIFAR_LITMUS_CROSS_XCD, "cross-xcd"),
+                                 (S.SIFAR_LITMUS_SAME_XCD, "same-xcd")):
+                for pairs in (8, 64, 256, 512):
+                    r = S.sifar_litmus(proto, place, pairs, trials)
+                    print(json.dumps({
+                        "workload": "litmus", "reader": pname, "placement": lname,
+                        "pairs": pairs, "trials": r["trials"], "violations": r["violations"],
+                        "violation_rate": r["violations"] / max(r["trials"], 1),
+                        "violations_first_epochs": r["violations_first_epochs"],
+                        "pairs_placed": r["pairs_placed"], "timeouts": r["timeouts"],
+                        "ns_per_trial": round(r["ns_per_trial"], 1),
+                        "first_violation": r["first_bad"]}), flush=True)
         return
     if args.workload == "smoke-n2":
         pts = [chain_point(synth.SMOKE_N2, 1, args)]

@@ -82,8 +82,9 @@ typedef struct sifar_ctx *sifar_t;
  *          epoch's payload was written by an earlier launch. It does not hold
  *          for a producer that is writing at that moment: measured on MI355X
  *          with producer and consumer on different XCDs, ~2 % of persistent
- *          all-reduces accepted a rank's previous epoch under a fresh stamp.
- *          So persistent steps refuse SPEC (SIFAR_EINVAL).
+ *          all-reduces accepted a rank's previous epoch under a fresh stamp
+ *          (sifar_litmus measures the same per handoff). So persistent steps
+ *          refuse SPEC (SIFAR_EINVAL).
  * ORDERED  stamps are read first and the payload is loaded only once all
  *          are fresh: a top barrier by flag polling (the "oneshot + dual
  *          buffering" configuration of Sec. 3.4). Correct without any
@@ -315,6 +316,52 @@ enum {
 };
 int sifar_floor(int32_t kind, int32_t iterations, void *stream, double *ns_per_op,
                 uint32_t info[4]);
+
+/* ---- Handoff litmus --------------------------------------------------------
+ * Checks the memory-model assumption the validation rests on (Sec. 4.2: a
+ * fresh stamp must imply fresh payload; Sec. 8.1 argues it for read-first
+ * loads) on this GPU. `pairs` producer/consumer wave pairs (a multiple of 8,
+ * 8..512) each pass one dual-buffered slot of 8 ranks x 64 lanes x 16 bytes
+ * through `trials` epochs (1..2^20), with the persistent step's primitives and
+ * slot discipline; the consumer compares every word it accepted with the epoch
+ * it validated.
+ *
+ *  protocol  SIFAR_LITMUS_ORDERED: stamps first, then (from another XCD) an
+ *            acquire, then the payload -- the persistent step's reader;
+ *            SIFAR_LITMUS_READ_FIRST: payload and stamps loaded together and
+ *            accepted when every stamp is fresh -- the paper's speculative
+ *            reader (a stale stamp leads to an acquire and a reload of both)
+ *  placement SIFAR_LITMUS_CROSS_XCD: producer and consumer on different XCDs;
+ *            SIFAR_LITMUS_SAME_XCD: on one XCD (workgroups are dealt to the 8
+ *            XCDs round robin; the waves read where they actually ran)
+ *
+ * On return *result holds the trials completed, the trials whose accepted
+ * payload held a word of another epoch (violations), how many of those were
+ * in the first two epochs (where the stale words are the slot's initial
+ * zeros rather than a rewritten epoch's), the bounded waits that
+ * gave up, how many pairs landed as asked, the consumers' mean nanoseconds per
+ * trial, and for the first violation {epoch, word found, word expected,
+ * (producer XCD << 8) | consumer XCD}. Synchronises `stream`; allocates and
+ * frees its own device memory (16 KiB per pair plus control words). Returns
+ * SIFAR_EINVAL for a bad argument, SIFAR_ENOMEM, SIFAR_EHIP, or SIFAR_EDEVICE
+ * when a wait gave up (the result is still filled in). Violations are data,
+ * not an error. */
+#define SIFAR_LITMUS_ORDERED 0
+#define SIFAR_LITMUS_READ_FIRST 1
+#define SIFAR_LITMUS_CROSS_XCD 0
+#define SIFAR_LITMUS_SAME_XCD 1
+typedef struct {
+    uint64_t trials;
+    uint64_t violations;
+    uint64_t violations_first_epochs;
+    uint64_t timeouts;
+    uint32_t pairs_placed;
+    uint32_t pairs;
+    double ns_per_trial;
+    uint32_t first_bad[4];
+} sifar_litmus_result;
+int sifar_litmus(int32_t protocol, int32_t placement, int32_t pairs, int32_t trials,
+                 void *stream, sifar_litmus_result *result);
 
 #ifdef __cplusplus
 }

@@ -53,6 +53,11 @@ SIFAR_FLOOR_RELEASE_FENCE = 7
 SIFAR_FLOOR_PINGPONG_XCD = 8
 SIFAR_FLOOR_PINGPONG_SAME_XCD = 9
 
+SIFAR_LITMUS_ORDERED = 0
+SIFAR_LITMUS_READ_FIRST = 1
+SIFAR_LITMUS_CROSS_XCD = 0
+SIFAR_LITMUS_SAME_XCD = 1
+
 CHUNK = 512  # elements per chunk (one 64-lane wave, 16 bytes per lane)
 
 # every symbol include/sifar.h declares
@@ -61,7 +66,21 @@ EXPORTS = (
     "sifar_produce", "sifar_reduce", "sifar_reduce_rmsnorm", "sifar_bind_step",
     "sifar_step", "sifar_set_injection", "sifar_log_geometry", "sifar_read_log",
     "sifar_epochs", "sifar_status", "sifar_error_info", "sifar_strerror", "sifar_floor",
+    "sifar_litmus",
 )
+
+
+class sifar_litmus_result(ctypes.Structure):
+    _fields_ = [
+        ("trials", ctypes.c_uint64),
+        ("violations", ctypes.c_uint64),
+        ("violations_first_epochs", ctypes.c_uint64),
+        ("timeouts", ctypes.c_uint64),
+        ("pairs_placed", ctypes.c_uint32),
+        ("pairs", ctypes.c_uint32),
+        ("ns_per_trial", ctypes.c_double),
+        ("first_bad", ctypes.c_uint32 * 4),
+    ]
 
 
 class sifar_config(ctypes.Structure):
@@ -144,6 +163,8 @@ def load(path: str = LIB_PATH):
         "sifar_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         "sifar_floor": (ctypes.c_int, [I32, I32, P, ctypes.POINTER(ctypes.c_double),
                                        ctypes.POINTER(U32)]),
+        "sifar_litmus": (ctypes.c_int, [I32, I32, I32, I32, P,
+                                        ctypes.POINTER(sifar_litmus_result)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -269,6 +290,20 @@ def sifar_floor(kind: int, iterations: int, stream=None):
     _check("sifar_floor", load().sifar_floor(kind, iterations, _stream(stream),
                                              ctypes.byref(ns), info))
     return ns.value, list(info)
+
+
+def sifar_litmus(protocol: int, placement: int, pairs: int, trials: int, stream=None) -> dict:
+    """Handoff litmus: returns the result fields as a dict. A bounded wait that
+    gave up raises (after the result was read back)."""
+    r = sifar_litmus_result()
+    rc = load().sifar_litmus(protocol, placement, pairs, trials, _stream(stream), ctypes.byref(r))
+    out = {name: getattr(r, name) for name, _ in sifar_litmus_result._fields_}
+    out["first_bad"] = list(r.first_bad)
+    if rc != SIFAR_OK:
+        err = SifarError("sifar_litmus", rc)
+        err.result = out
+        raise err
+    return out
 
 
 def sifar_status(h: int) -> int:

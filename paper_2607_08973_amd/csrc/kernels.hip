@@ -17,7 +17,8 @@
 //    to accept stale data.
 //
 // Memory-model choices (LLVM AMDGPU memory model for GFX942/950; the 8 XCDs
-// have separate L2s, so agent scope means "coherent across XCDs"):
+// have separate L2s, so agent scope means "coherent across XCDs"; the handoff
+// primitives live in coherence.h, which the handoff litmus also runs):
 //  - stamps are read with agent-scope atomic loads;
 //  - per-epoch SPEC issues the payload loads and the stamp loads together (the
 //    paper's concurrent payload warps and validation warp); ORDERED acquires
@@ -33,35 +34,11 @@
 // Arithmetic: fp32 adds in ascending rank order (no reassociation, no FMA
 // contraction), bf16 rounding by the native V_CVT_PK_BF16_F32 (round to nearest
 // even, fp32 denormals enabled).
+#include "coherence.h"
 #include "sifar_kernels.h"
 
 namespace sifar {
 namespace {
-
-struct alignas(16) V16 {
-    uint32_t w[4];
-};
-
-__device__ __forceinline__ V16 ld16(const uint16_t *p) {
-    return *reinterpret_cast<const V16 *>(p);
-}
-
-// 16 bytes as two agent-scope atomic loads: coherent across the XCDs' L2s.
-__device__ __forceinline__ V16 ld16_agent(const uint16_t *p) {
-    const uint64_t *q = reinterpret_cast<const uint64_t *>(p);
-    const uint64_t a = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint64_t b = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    V16 v;
-    v.w[0] = static_cast<uint32_t>(a);
-    v.w[1] = static_cast<uint32_t>(a >> 32);
-    v.w[2] = static_cast<uint32_t>(b);
-    v.w[3] = static_cast<uint32_t>(b >> 32);
-    return v;
-}
-
-__device__ __forceinline__ void st16(uint16_t *p, const V16 &v) {
-    *reinterpret_cast<V16 *>(p) = v;
-}
 
 __device__ __forceinline__ float lo_f32(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_f32(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
@@ -71,39 +48,6 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
     const __bf16 b = static_cast<__bf16>(hi);
     return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
            (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
-}
-
-__device__ __forceinline__ uint32_t ld_relaxed(const uint32_t *p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ uint32_t ld_acquire(const uint32_t *p) {
-    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ void st_relaxed(uint32_t *p, uint32_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// A flag for a partner wave on this XCD: a plain store lands in the XCD's L2,
-// where the partner's agent-scope loads read it; an agent-scope store is
-// written past the L2 and becomes visible to a poller later.
-__device__ __forceinline__ void st_flag(uint32_t *p, uint32_t v, bool local) {
-    if (local)
-        __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    else
-        __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ void st_release(uint32_t *p, uint32_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Makes every load that fed `v` complete before any later instruction issues:
-// the value is consumed by an (empty) compiler barrier, so the compiler must
-// wait for it there.
-__device__ __forceinline__ void complete(const V16 &v) {
-    asm volatile("" ::"v"(v.w[0]), "v"(v.w[1]), "v"(v.w[2]), "v"(v.w[3]) : "memory");
 }
 
 __device__ __forceinline__ uint32_t epoch_of(const EpochRef &e) { return e.base[0] + e.off; }
@@ -122,7 +66,6 @@ __device__ void latch(uint32_t *err, uint32_t kind, uint32_t g, uint32_t c, uint
 __device__ __forceinline__ bool latched(const uint32_t *err) { return ld_relaxed(err) != 0; }
 
 constexpr uint32_t kErrRetryBudget = 1, kErrWaw = 2, kErrExchange = 3;
-constexpr uint32_t kPlaceSpins = 1u << 14;  // polls for a partner wave's placement tag
 
 // Where the calling lane works: token t, chunk s of the row, chunk index c.
 // Lanes past the end of the row load a clamped, in-bounds address and do not
@@ -170,74 +113,6 @@ __device__ __forceinline__ void copy_chunk(const ProduceArgs &a, const Chunk &k,
     if (k.lane_ok) {
 #pragma unroll
         for (int r = 0; r < N; ++r) st16(dst + r * 2 * geo.slot_elems, v[r]);
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Placement of a persistent step's waves. Workgroups are dealt to the 8 XCDs
-// round robin, so a chunk's consumer and producer share an XCD when the
-// plane offset is a multiple of 8 -- but the kernel reads where it runs
-// (XCC_ID) instead of assuming it. At step start every wave publishes
-// ((base + 1) << 32) | 0x100 | XCD for its chunk and plane; a wave then reads
-// its partner's tag (bounded wait; a missing tag counts as another XCD).
-
-__device__ __forceinline__ uint32_t xcc_id() {
-    uint32_t v;
-    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID, 0, 4)" : "=s"(v));
-    return v;
-}
-
-__device__ __forceinline__ uint64_t place_tag(uint32_t base, uint32_t xcc) {
-    return (static_cast<uint64_t>(base + 1u) << 32) | 0x100u | xcc;
-}
-
-__device__ __forceinline__ void publish_place(uint64_t *place, uint32_t base, int lane) {
-    if (lane == 0)
-        __hip_atomic_store(place, place_tag(base, xcc_id()), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Wave-uniform: does the partner wave whose tag is *place run on this XCD?
-__device__ __forceinline__ bool partner_is_local(const uint64_t *place, uint32_t base, int lane) {
-    uint32_t local = 0;
-    if (lane == 0) {
-        const uint64_t want = place_tag(base, xcc_id());
-        uint64_t t = 0;
-        for (uint32_t spins = 0; spins < kPlaceSpins; ++spins) {
-            t = __hip_atomic_load(place, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if ((t >> 32) == (want >> 32)) break;
-            __builtin_amdgcn_s_sleep(1);
-        }
-        local = t == want ? 1u : 0u;
-    }
-    return __builtin_amdgcn_readfirstlane(local) != 0;
-}
-
-// Per lane: does the wave whose tag is *place run on this XCD? (bounded wait)
-__device__ __forceinline__ bool tag_is_local(const uint64_t *place, uint32_t base) {
-    const uint64_t want = place_tag(base, xcc_id());
-    uint64_t t = 0;
-    for (uint32_t spins = 0; spins < kPlaceSpins; ++spins) {
-        t = __hip_atomic_load(place, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if ((t >> 32) == (want >> 32)) break;
-        __builtin_amdgcn_s_sleep(1);
-    }
-    return t == want;
-}
-
-// Publication of a producer's slot stores before its stamps. To a consumer on
-// another XCD: an agent-scope release fence, which writes back this XCD's L2.
-// To a consumer on this XCD: waiting until the stores have reached the L2 is
-// enough, because the L2 is the point of coherence of all CUs of one XCD and
-// the consumer's agent-scope loads bypass its CU's L1 (the threadgroup-split
-// workgroup scope of the LLVM AMDGPU memory model rests on the same fact: its
-// release waits for the stores, its acquire bypasses or invalidates L1).
-__device__ __forceinline__ void publish_slot(bool local) {
-    if (local) {
-        __builtin_amdgcn_s_waitcnt(0);
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    } else {
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     }
 }
 
@@ -387,10 +262,7 @@ __device__ __forceinline__ void gather_chain(const ReduceArgs &a, const Chunk &k
         last = m;
         fail = m != 0 || attempts <= a.forced_retries;
     }
-    if (local)
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    else
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    acquire_slot(local);
     load_payload<N, true>(v, slot0, rank_step);
 }
 

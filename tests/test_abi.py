@@ -116,3 +116,14 @@ def test_floor_rejects_bad_arguments_on_host(kind, iterations):
     assert L.sifar_floor(kind, iterations, None, ctypes.byref(ns), info) == S.SIFAR_EINVAL
     assert L.sifar_floor(S.SIFAR_FLOOR_ATOMIC, 10, None, None, info) == S.SIFAR_EINVAL
     assert L.sifar_floor(S.SIFAR_FLOOR_ATOMIC, 10, None, ctypes.byref(ns), None) == S.SIFAR_EINVAL
+
+
+@pytest.mark.parametrize("protocol,placement,pairs,trials", [
+    (2, 0, 8, 10), (-1, 0, 8, 10), (0, 2, 8, 10), (0, 0, 0, 10), (0, 0, 12, 10),
+    (0, 0, 520, 10), (0, 0, 8, 0), (0, 0, 8, (1 << 20) + 1),
+])
+def test_litmus_rejects_bad_arguments(protocol, placement, pairs, trials):
+    L = S.load()
+    r = S.sifar_litmus_result()
+    assert L.sifar_litmus(protocol, placement, pairs, trials, None, ctypes.byref(r)) == S.SIFAR_EINVAL
+    assert L.sifar_litmus(0, 0, 8, 10, None, None) == S.SIFAR_EINVAL
