@@ -141,29 +141,34 @@ __device__ void consumer(const LitmusArgs &a, int pair, int lane) {
 #pragma unroll
         for (int r = 0; r < kLitmusRanks; ++r) complete(v[r]);
         if (lane == 0) st_flag(a.consumed + pc, g, local);
-        uint32_t found = 0, want = 0;
-        bool wrong = false;
+        // branch-free test first (it stays off the handoff's critical path);
+        // the first wrong word is looked up only when there is one
+        uint32_t diff = 0;
 #pragma unroll
         for (int r = 0; r < kLitmusRanks; ++r)
 #pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                const uint32_t e = value_of(g, r, lane, w);
-                if (!wrong && v[r].w[w] != e) {
-                    wrong = true;
-                    found = v[r].w[w];
-                    want = e;
-                }
-            }
+            for (int w = 0; w < 4; ++w) diff |= v[r].w[w] ^ value_of(g, r, lane, w);
+        const bool wrong = diff != 0;
         const uint64_t m = __ballot(wrong);
         ++done;
         if (m != 0) {
-            const int src = __builtin_ctzll(m);
-            found = __shfl(found, src);
-            want = __shfl(want, src);
             if (bad == 0) {
+                uint32_t found = 0, want = 0;
+                bool hit = false;
+#pragma unroll
+                for (int r = 0; r < kLitmusRanks; ++r)
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) {
+                        const uint32_t e = value_of(g, r, lane, w);
+                        const bool first = !hit && v[r].w[w] != e;
+                        found = first ? v[r].w[w] : found;
+                        want = first ? e : want;
+                        hit = hit || first;
+                    }
+                const int src = __builtin_ctzll(m);
                 bad_g = g;
-                bad_found = found;
-                bad_want = want;
+                bad_found = __shfl(found, src);
+                bad_want = __shfl(want, src);
             }
             ++bad;
             if (g <= 2) ++bad_early;
