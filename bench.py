@@ -168,7 +168,7 @@ def parse():
     ap.add_argument("--floor-nodes", type=int, default=64)
     ap.add_argument("--workload", default="llama8b-decode",
                     choices=["llama8b-decode", "smoke-n2", "spec-stress", "sweep", "moe-rmsnorm",
-                             "ablation", "retry-curve", "reduce-cold", "litmus"],
+                             "ablation", "retry-curve", "reduce-cold", "litmus", "misspec-vs-tp"],
                     help="llama8b-decode is the headline line; the others print one "
                          "JSON line per configuration")
     ap.add_argument("--wpg", type=int, default=1, choices=[1, 2, 4, 8, 16],
@@ -483,6 +483,17 @@ def suite(args):
             pt = chain_point(wp, 4, args, inject=prob > 0)
             pt.update(stale_prob=prob)
             pts.append(pt)
+    elif args.workload == "misspec-vs-tp":
+        # how often a chunk's first stamp poll finds a rank not yet published,
+        # by TP degree, with no injection (the paper's mis-speculation rate
+        # grows with TP, Sec. 6.3): in a persistent step the emulated peers
+        # run concurrently with the reduction, so this is their natural lag
+        w0 = synth.LLAMA8B_DECODE
+        pts = []
+        for N in (2, 4, 8):
+            w = dataclasses.replace(w0, nranks=N, name=f"llama8b-decode-n{N}-h4096-chain64")
+            for T in w.tokens:
+                pts.append(chain_point(w, T, args, T_max=max(w.tokens)))
     elif args.workload == "moe-rmsnorm":
         w = synth.MOE_DECODE
         pts = []
