@@ -106,6 +106,15 @@ typedef struct sifar_ctx *sifar_t;
  * The resulting per-chunk decisions are exactly predictable (see the log). */
 #define SIFAR_INJECT_OFF 0
 #define SIFAR_INJECT_DETERMINISTIC 1
+/* SLOT_OVERRUN: the host stops refusing a sifar_produce that would rewrite a
+ * slot whose epoch has not been reduced yet (the dual-buffer limit, Sec. 4.1),
+ * so a test can force the write-after-write hazard that dual buffering
+ * removes. The producer kernel's own check must then latch SIFAR_DEV_WAW, and
+ * the overwritten epoch's reduction sees fresh stamps of another epoch, so it
+ * exhausts max_attempts. `table` and `entries` are ignored; an installed
+ * DETERMINISTIC table stays installed. Eager calls only (a step needs every
+ * produced epoch reduced first). SIFAR_INJECT_OFF ends it. */
+#define SIFAR_INJECT_SLOT_OVERRUN 2
 
 /* ---- configuration ---------------------------------------------------------- */
 typedef struct {
@@ -235,8 +244,9 @@ int sifar_step(sifar_t h, int32_t tokens, void *stream);
 /* ---- injection, logs, state --------------------------------------------------- */
 
 /* Install (copies) a host table of `entries` uint16 words (late | withheld << 8)
- * for `mode`; SIFAR_INJECT_OFF clears it. Rank bits >= N are ignored. Drops
- * captured graphs. Not allowed with SIFAR_VALIDATE_NONE. */
+ * for `mode` DETERMINISTIC, or switch on SLOT_OVERRUN; SIFAR_INJECT_OFF clears
+ * both. Rank bits >= N are ignored. Drops captured graphs. Not allowed with
+ * SIFAR_VALIDATE_NONE. */
 int sifar_set_injection(sifar_t h, const uint16_t *table, int32_t entries, int32_t mode);
 
 /* Decision log geometry: the log is a ring of log_epochs rows of w_max words;

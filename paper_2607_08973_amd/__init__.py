@@ -40,6 +40,7 @@ VALIDATE = {"spec": 0, "ordered": 1, "none": 2}
 
 SIFAR_INJECT_OFF = 0
 SIFAR_INJECT_DETERMINISTIC = 1
+SIFAR_INJECT_SLOT_OVERRUN = 2
 
 # latency floors (sifar_floor kinds)
 SIFAR_FLOOR_GRAPH_NODE = 0
@@ -249,6 +250,9 @@ def sifar_step(h: int, tokens: int, stream=None) -> None:
 
 
 def sifar_set_injection(h: int, table: Optional[Sequence[int]], mode: int) -> None:
+    if mode == SIFAR_INJECT_SLOT_OVERRUN:
+        _check("sifar_set_injection", load().sifar_set_injection(h, None, 0, mode))
+        return
     if table is None or mode == SIFAR_INJECT_OFF:
         _check("sifar_set_injection", load().sifar_set_injection(h, None, 0, SIFAR_INJECT_OFF))
         return

@@ -32,6 +32,7 @@ struct sifar_ctx {
     DevState *state = nullptr;
     uint16_t *inject = nullptr;
     int32_t inject_entries = 0;
+    bool slot_overrun = false;     // SIFAR_INJECT_SLOT_OVERRUN: no host dual-buffer limit
 
     uint32_t next_prod = 1, next_red = 1;
     int32_t prod_tokens[2] = {0, 0};
@@ -407,8 +408,9 @@ int sifar_produce(sifar_t h, const void *src, int64_t src_rank_stride, int32_t t
     if (!src || !aligned16(src) || tokens < 1 || tokens > h->cfg.max_tokens) return SIFAR_EINVAL;
     if (src_rank_stride % 8 || src_rank_stride < static_cast<int64_t>(tokens) * h->cfg.hidden)
         return SIFAR_EINVAL;
-    // every slot holds an unreduced epoch
-    if (h->next_prod - h->next_red >= static_cast<uint32_t>(h->cfg.buffers)) return SIFAR_ESTATE;
+    // every slot holds an unreduced epoch (unless a test forces the overwrite)
+    if (!h->slot_overrun && h->next_prod - h->next_red >= static_cast<uint32_t>(h->cfg.buffers))
+        return SIFAR_ESTATE;
     const uint32_t g = h->next_prod;
     const EpochRef ep{&h->state->zero, g, g & parity_mask(h)};
     ProduceArgs pa = produce_args(h, tokens, ep, static_cast<const uint16_t *>(src), 0,
@@ -540,11 +542,16 @@ int sifar_set_injection(sifar_t h, const uint16_t *table, int32_t entries, int32
         (void)hipFree(h->inject);
         h->inject = nullptr;
         h->inject_entries = 0;
+        h->slot_overrun = false;
         drop_graphs(h);
         return SIFAR_OK;
     }
-    if (mode != SIFAR_INJECT_DETERMINISTIC) return SIFAR_EINVAL;
+    if (mode != SIFAR_INJECT_DETERMINISTIC && mode != SIFAR_INJECT_SLOT_OVERRUN) return SIFAR_EINVAL;
     if (h->cfg.validate == SIFAR_VALIDATE_NONE) return SIFAR_EINVAL;
+    if (mode == SIFAR_INJECT_SLOT_OVERRUN) {
+        h->slot_overrun = true;
+        return SIFAR_OK;
+    }
     if (!table || entries < 1) return SIFAR_EINVAL;
     if (hipDeviceSynchronize() != hipSuccess) return SIFAR_EHIP;
     uint16_t *d = nullptr;

@@ -127,3 +127,48 @@ def test_litmus_rejects_bad_arguments(protocol, placement, pairs, trials):
     r = S.sifar_litmus_result()
     assert L.sifar_litmus(protocol, placement, pairs, trials, None, ctypes.byref(r)) == S.SIFAR_EINVAL
     assert L.sifar_litmus(0, 0, 8, 10, None, None) == S.SIFAR_EINVAL
+
+
+def test_every_numeric_define_matches_the_binding():
+    text = open(HEADER).read()
+    defs = re.findall(r"#define (SIFAR_\w+)\s+\(?(-?\d+)\)?", text)
+    assert len(defs) >= 15
+    for k, v in defs:
+        assert getattr(S, k) == int(v), k
+
+
+def test_litmus_result_layout_matches_header():
+    text = open(HEADER).read()
+    body = re.search(r"typedef struct \{([^{}]*)\} sifar_litmus_result;", text).group(1)
+    fields = re.findall(r"\b(\w+)(?:\[\d+\])?;", body)
+    assert fields == [f for f, _ in S.sifar_litmus_result._fields_]
+    assert ctypes.sizeof(S.sifar_litmus_result) == 4 * 8 + 2 * 4 + 8 + 4 * 4
+
+
+def test_struct_offsets_match_a_c_compiler(tmp_path):
+    """The ctypes mirrors against what a C compiler makes of the header."""
+    import shutil
+    import subprocess
+
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    structs = {"sifar_config": S.sifar_config, "sifar_step_buffers": S.sifar_step_buffers,
+               "sifar_litmus_result": S.sifar_litmus_result}
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "sifar.h"', "int main(void) {"]
+    for name, cls in structs.items():
+        lines.append(f'    printf("{name} size %zu\\n", sizeof({name}));')
+        for f, _ in cls._fields_:
+            lines.append(f'    printf("{name} {f} %zu\\n", offsetof({name}, {f}));')
+    lines += ["    return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-std=c11", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)],
+                   check=True)
+    got = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    for line in filter(None, got):
+        name, what, value = line.split()
+        cls = structs[name]
+        want = ctypes.sizeof(cls) if what == "size" else getattr(cls, what).offset
+        assert int(value) == want, line

@@ -174,6 +174,50 @@ def test_withheld_stamp_exhausts_budget():
     s.close()
 
 
+@pytest.mark.parametrize("validate", ["spec", "ordered"])
+def test_forced_slot_overrun_is_caught(validate):
+    """The hazard dual buffering exists to prevent (Sec. 4.1), forced from the
+    host: epoch 3 is produced into epoch 1's slot before epoch 1 is reduced.
+    The producer's check latches the WAW error, and the reduction of epoch 1,
+    which now finds epoch 3's stamps, never validates: its output is not
+    epoch 1's sum."""
+    N, T, H = 2, 1, 1024
+    pool = synth.payload_pool(9, N, T, H, 3, "normal")
+    src = to_dev(pool)
+    out = torch.zeros((T, H), dtype=torch.int16, device=DEV)
+    s = S.Sifar(nranks=N, hidden=H, max_tokens=T, reduces_per_step=2, max_attempts=4,
+                validate=validate, log_epochs=4)
+    s.set_injection(None, S.SIFAR_INJECT_SLOT_OVERRUN)
+    s.produce(src[0], T)
+    s.produce(src[1], T)
+    s.produce(src[2], T)       # rewrites epoch 1's slot
+    s.reduce(out, T)           # epoch 1
+    log = s.read_log()
+    assert s.status() == S.SIFAR_EDEVICE
+    kind, epoch, chunk, prev = s.error_info()
+    assert (kind, epoch, prev) == (S.SIFAR_DEV_WAW, 3, 1)
+    segs = (H + 511) // 512
+    assert np.all(log[0, :segs] & 0xFFFF == 4)               # budget spent
+    assert np.all((log[0, :segs] >> 24) == 0b11)             # both ranks stale at the end
+    assert not np.array_equal(to_host(out), oracle.reduce(pool[0]))
+    s.close()
+
+
+def test_slot_overrun_mode_off_restores_the_limit():
+    N, T, H = 2, 1, 512
+    pool = synth.payload_pool(10, N, T, H, 3, "normal")
+    src = to_dev(pool)
+    with S.Sifar(nranks=N, hidden=H, max_tokens=T, reduces_per_step=2) as s:
+        s.set_injection(None, S.SIFAR_INJECT_SLOT_OVERRUN)
+        s.set_injection(None, S.SIFAR_INJECT_OFF)
+        s.produce(src[0], T)
+        s.produce(src[1], T)
+        with pytest.raises(S.SifarError) as e:
+            s.produce(src[2], T)
+        assert e.value.code == S.SIFAR_ESTATE
+        s.check()
+
+
 def test_protocol_order_errors():
     N, T, H = 2, 1, 512
     pool = synth.payload_pool(8, N, T, H, 4, "normal")
