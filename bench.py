@@ -55,8 +55,9 @@ def produce_bytes(N: int, T: int, H: int) -> int:
 def latency_floors() -> dict:
     """The library's latency probes (sifar_floor): launch and graph-node
     floors, one agent-scope atomic, acquire / coherent / warm / cache-missing
-    load, a release fence after a store, and a release -> acquire handoff
-    across and within an XCD."""
+    load, a release fence after a store, a release -> acquire handoff across
+    and within an XCD; and the dual-buffered slot loop of the handoff litmus
+    (sifar_litmus), per epoch."""
     import paper_2607_08973_amd as S
 
     probes = (  # (name in the JSON line, kind, operations, scale from ns)
@@ -77,6 +78,13 @@ def latency_floors() -> dict:
         out[name] = round(ns * scale, 4 if scale != 1.0 else 1)
         if kind in (S.SIFAR_FLOOR_PINGPONG_XCD, S.SIFAR_FLOOR_PINGPONG_SAME_XCD):
             out[name.replace("_ns", "_xccs")] = info[1:3]
+    # the persistent step's own per-chunk loop (dual-buffered slot, stamps,
+    # release of the slot) with nothing else in it: 8 producer/consumer pairs,
+    # as many as the chunks of one 4096-wide token
+    for name, place in (("slot_loop_same_xcd_ns", S.SIFAR_LITMUS_SAME_XCD),
+                        ("slot_loop_cross_xcd_ns", S.SIFAR_LITMUS_CROSS_XCD)):
+        r = S.sifar_litmus(S.SIFAR_LITMUS_ORDERED, place, 8, 65536)
+        out[name] = round(r["ns_per_trial"], 1)
     return out
 
 
