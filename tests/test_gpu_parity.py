@@ -360,6 +360,45 @@ def test_epilogue_moe_chain(T, waves_per_group, fuse):
     print(f"epilogue T={T} G={waves_per_group}: max y distance {worst} step(s)")
 
 
+@pytest.mark.parametrize("N,T,H,persistent,G", [
+    (8, 3, 65536, 0, 2), (3, 2, 65528, 0, 2),    # per launch: 64 groups of 2 waves per token
+    (8, 3, 32768, 1, 1), (3, 2, 32760, 1, 1),    # persistent: 64 one-wave groups per token
+])
+def test_epilogue_widest_rows(N, T, H, persistent, G):
+    """Residual-add + RMSNorm at the widest rows each kind of step takes: the
+    per-token sum of squares is exchanged between 64 workgroups, one word per
+    lane of the polling wave, the most it holds; full and ragged last chunks;
+    8 chained nodes, two steps."""
+    w = synth.Workload(90 + N, f"epilogue-n{N}-h{H}", N, (T,), H, 8, 2, "act",
+                       epilogue=True)
+    # a 5-entry source pool: epochs reuse entries cyclically
+    run = StepRun(w, T, persistent=persistent, waves_per_group=G,
+                  pool=synth.payload_pool(w.wid, N, T, H, 5, w.dist))
+    res = run.res0[:T].copy()
+    for step in range(2):
+        epochs = run.step(T)
+        y_got = to_host(run.y_d)
+        _, r_list, y_list = oracle.reduce_chain(run.pool, epochs, T,
+                                                epilogue=(res, run.weight, w.rms_eps))
+        assert np.array_equal(to_host(run.res_d)[:T], r_list[-1])
+        for i in range(w.reduces_per_step):
+            assert ulp_distance(y_got[i, :T], y_list[i]).max() <= 1, f"step {step} node {i}"
+        res = r_list[-1]
+    run.s.check()
+    run.s.close()
+
+
+@pytest.mark.parametrize("H,persistent,G", [(65536, 0, 1), (32776, 1, 1), (65536, 1, 4)])
+def test_epilogue_rows_beyond_the_exchange_are_refused(H, persistent, G):
+    """More than 64 groups per token (or, persistent, more than 64 chunks) would
+    not fit the one-word-per-lane exchange: refused at init."""
+    with pytest.raises(S.SifarError) as e:
+        S.Sifar(nranks=8, hidden=H, max_tokens=2, reduces_per_step=2, epilogue=1,
+                waves_per_group=G, persistent=persistent,
+                validate="ordered" if persistent else "spec")
+    assert e.value.code == S.SIFAR_EINVAL
+
+
 def test_epilogue_residual_chain_every_node_eager():
     """Eager fused calls: the residual after every node, bit-exact."""
     N, T, H = 8, 3, 8192
