@@ -22,16 +22,41 @@ __device__ __forceinline__ V16 ld16(const uint16_t *p) {
     return *reinterpret_cast<const V16 *>(p);
 }
 
-// 16 bytes as two agent-scope atomic loads: coherent across the XCDs' L2s.
-__device__ __forceinline__ V16 ld16_agent(const uint16_t *p) {
-    const uint64_t *q = reinterpret_cast<const uint64_t *>(p);
-    const uint64_t a = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint64_t b = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// `p`, the same in every lane of the wave, as a value the compiler knows to be
+// wave-uniform (a scalar register pair), as a buffer descriptor needs.
+// readfirstlane yields an int, so each half is taken as uint32_t: a low word
+// with bit 31 set must not be sign-extended into the high word.
+__device__ __forceinline__ const void *uniform_ptr(const void *p) {
+    const uint64_t v = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo =
+        static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v)));
+    const uint32_t hi =
+        static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32)));
+    return reinterpret_cast<const void *>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// Buffer descriptor word 3 on gfx9-family GPUs: 32-bit data format, no
+// swizzle, no thread-id addressing.
+constexpr int32_t kBufferWord3 = 0x00020000;
+// Cache policy of a buffer load: SC1 set, SC0 clear = agent scope.
+constexpr int32_t kCachePolicyAgent = 16;
+
+// 16 bytes at byte offset `off` (per lane, below 2^31) from `base` (the same
+// in every lane of the wave) with the agent-scope cache policy: the load
+// bypasses this CU's L1 and is served by the XCD's L2 or memory -- the caching
+// of an agent-scope atomic load, in one 16-byte load instead of two 8-byte
+// ones.
+__device__ __forceinline__ V16 ld16_agent(const void *base, uint32_t off) {
+    typedef int v4i __attribute__((ext_vector_type(4)));
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<void *>(uniform_ptr(base)), 0, 0x7fffffff, kBufferWord3);
+    const v4i x = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0,
+                                                        kCachePolicyAgent);
     V16 v;
-    v.w[0] = static_cast<uint32_t>(a);
-    v.w[1] = static_cast<uint32_t>(a >> 32);
-    v.w[2] = static_cast<uint32_t>(b);
-    v.w[3] = static_cast<uint32_t>(b >> 32);
+    v.w[0] = static_cast<uint32_t>(x[0]);
+    v.w[1] = static_cast<uint32_t>(x[1]);
+    v.w[2] = static_cast<uint32_t>(x[2]);
+    v.w[3] = static_cast<uint32_t>(x[3]);
     return v;
 }
 

@@ -165,11 +165,10 @@ __global__ __launch_bounds__(1024) void produce_kernel(ProduceArgs a) {
 // ---------------------------------------------------------------------------
 // Consumer side.
 
-template <int N, bool AGENT>
+template <int N>
 __device__ __forceinline__ void load_payload(V16 (&v)[N], const uint16_t *slot0, uint64_t rank_step) {
 #pragma unroll
-    for (int r = 0; r < N; ++r) v[r] = AGENT ? ld16_agent(slot0 + r * rank_step)
-                                             : ld16(slot0 + r * rank_step);
+    for (int r = 0; r < N; ++r) v[r] = ld16(slot0 + r * rank_step);
 }
 
 // Gather of a per-epoch launch: load chunk k of epoch g, validate its N
@@ -190,7 +189,7 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
     if (MODE == kOrdered) {
         if (k.active && lane < N) st = ld_acquire(stamp + lane);
     } else {
-        load_payload<N, false>(v, slot0, rank_step);
+        load_payload<N>(v, slot0, rank_step);
         if (MODE == kSpec && k.active && lane < N) st = ld_relaxed(stamp + lane);
     }
 
@@ -217,7 +216,7 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
                 if (lane < N) st = ld_acquire(stamp + lane);
             } else {
                 if (lane < N) st = ld_relaxed(stamp + lane);
-                load_payload<N, false>(v, slot0, rank_step);
+                load_payload<N>(v, slot0, rank_step);
             }
             ++attempts;
             m = static_cast<uint32_t>(__ballot(lane < N && st != g));
@@ -225,7 +224,7 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
             fail = m != 0 || attempts <= a.forced_retries;
         }
     }
-    if (MODE == kOrdered) load_payload<N, false>(v, slot0, rank_step);
+    if (MODE == kOrdered) load_payload<N>(v, slot0, rank_step);
 }
 
 // Persistent-step gather of an active chunk: a producer may be writing right
@@ -240,7 +239,12 @@ __device__ __forceinline__ void gather_chain(const ReduceArgs &a, const Chunk &k
                                              uint32_t &attempts, uint32_t &first,
                                              uint32_t &last, bool local) {
     const Geometry &geo = a.geo;
-    const uint16_t *slot0 = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + k.row;
+    // the chunk's first element in rank 0's slot (wave-uniform) and this
+    // lane's byte offset from it
+    const uint64_t row0 = static_cast<uint64_t>(k.t) * geo.hidden +
+                          static_cast<uint64_t>(k.s) * kChunk;
+    const uint16_t *chunk0 = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + row0;
+    const uint32_t off = static_cast<uint32_t>(k.row - row0) * 2u;
     const uint64_t rank_step = 2 * geo.slot_elems;  // slots are [rank][parity]
     const uint32_t *stamp = a.stamps + (static_cast<size_t>(p) * geo.w_max + k.c) * N;
     attempts = 1;
@@ -263,7 +267,8 @@ __device__ __forceinline__ void gather_chain(const ReduceArgs &a, const Chunk &k
         fail = m != 0 || attempts <= a.forced_retries;
     }
     acquire_slot(local);
-    load_payload<N, true>(v, slot0, rank_step);
+#pragma unroll
+    for (int r = 0; r < N; ++r) v[r] = ld16_agent(chunk0 + r * rank_step, off);
 }
 
 // Fixed-order fp32 sum: acc = x_0; acc += x_1; ... acc += x_{N-1}; then bf16.

@@ -97,7 +97,7 @@ __device__ __forceinline__ void load_slot(const LitmusArgs &a, int pair, uint32_
                                           V16 (&v)[kLitmusRanks]) {
 #pragma unroll
     for (int r = 0; r < kLitmusRanks; ++r)
-        v[r] = ld16_agent(reinterpret_cast<const uint16_t *>(slot_of(a, pair, p, r, lane)));
+        v[r] = ld16_agent(slot_of(a, pair, p, r, 0), static_cast<uint32_t>(lane) * 16u);
 }
 
 __device__ void consumer(const LitmusArgs &a, int pair, int lane) {
