@@ -214,6 +214,52 @@ def cpu_baseline(pool, tokens, budget_s):
     return mean_us, per_t
 
 
+def cpu_baseline_parallel(pool, tokens, budget_s, threads):
+    """The same C oracle entry point driven from up to `threads` host threads,
+    each reducing one contiguous slice of the T x H elements in place (the
+    oracle takes the rank stride and the element count separately). Slices
+    hold at least 8192 elements: a Python thread hand-off costs tens of
+    microseconds, more than a smaller slice's work. Checked once against the
+    single-threaded call."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+    import oracle
+
+    lib = oracle.lib()
+    per_t = {}
+    with ThreadPoolExecutor(threads) as ex:
+        for T in tokens:
+            xs = [np.ascontiguousarray(pool[e][:, :T]) for e in range(8)]
+            outs = [np.empty(x.shape[1:], np.uint16) for x in xs]
+            n_ranks, count = xs[0].shape[0], xs[0][0].size
+            parts = max(1, min(threads, count // 8192))
+            cuts = np.linspace(0, count, parts + 1).astype(np.int64)
+            spans = [(int(a), int(b)) for a, b in zip(cuts[:-1], cuts[1:]) if b > a]
+
+            def reduce_all(x, o):
+                def one(span):
+                    i0, i1 = span
+                    lib.oracle_reduce(x.ctypes.data + 2 * i0, n_ranks, count, i1 - i0,
+                                      o.ctypes.data + 2 * i0)
+                if len(spans) == 1:
+                    one(spans[0])
+                else:
+                    list(ex.map(one, spans))
+
+            reduce_all(xs[0], outs[0])
+            assert np.array_equal(outs[0], oracle.reduce(xs[0]))
+            n, t0 = 0, time.perf_counter()
+            while True:
+                reduce_all(xs[n % len(xs)], outs[n % len(xs)])
+                n += 1
+                el = time.perf_counter() - t0
+                if el > budget_s / len(tokens):
+                    break
+            per_t[T] = (el / n * 1e6, len(spans))
+    return sum(v for v, _ in per_t.values()) / len(per_t), per_t
+
+
 def host_cpu() -> str:
     """Model name of the host CPU and the cores this process may use."""
     model = "unknown CPU"
@@ -653,6 +699,21 @@ def main():
                          f"entries at batch {list(tokens)} for {args.cpu_seconds:.0f} s total; mean "
                          f"over batch sizes of per-reduce time: " +
                          ", ".join(f"T={t}: {v:.1f} us" for t, v in cpu_t.items())}
+        try:
+            avail = len(os.sched_getaffinity(0))
+        except (AttributeError, OSError):
+            avail = os.cpu_count() or 1
+        threads = max(1, min(avail, int(os.environ.get("OMP_NUM_THREADS", "16")), 16))
+        par_us, par_t = cpu_baseline_parallel(pool, tokens, args.cpu_seconds / 3, threads)
+        cpu["parallel"] = {
+            "value": round(par_us, 3), "unit": "us per all-reduce",
+            "cores": max(k for _, k in par_t.values()),
+            "sample": f"the same oracle entry point on up to {threads} threads (cores = the "
+                      f"most it used), each a "
+                      f"contiguous slice of at least 8192 of the T x H elements, "
+                      f"{args.cpu_seconds / 3:.0f} s total: " +
+                      ", ".join(f"T={t}: {v:.1f} us on {k} thread(s)"
+                                for t, (v, k) in par_t.items())}
 
     s.close()
     rec = {
@@ -671,7 +732,9 @@ def main():
         "config": {"workload": w.name, "nranks": N, "hidden": H, "tokens": list(tokens),
                    "reduces_per_step": L, "validate": args.mode, "fuse_peers": args.fuse,
                    "persistent": args.persistent, "buffers": args.buffers,
-                   "step": f"{len(tokens)} captured decode steps of {L} all-reduces"},
+                   "step": (f"{len(tokens)} decode steps of {L} all-reduces, one persistent "
+                            f"launch each" if args.persistent else
+                            f"{len(tokens)} captured decode-step graphs of {L} all-reduces")},
         "reduces_per_s": round(1e6 / us_per_reduce, 1),
         "us_per_reduce_by_tokens": {str(k): round(v, 4) for k, v in per_t.items()},
         "dominant_kernel": {str(k): {kk: (round(vv, 4) if isinstance(vv, float) else vv)
@@ -681,6 +744,9 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
                      "traffic": traffic, "bytes_per_launch": round(mean_bytes),
+                     "residency": "warm: each epoch's slots were just written by the same "
+                                  "step's producer waves (cold reduction rates: "
+                                  "--workload reduce-cold)",
                      "launch_period_us": round(mean_period, 4)},
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
