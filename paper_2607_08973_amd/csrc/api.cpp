@@ -26,7 +26,7 @@ struct sifar_ctx {
     uint32_t *consumed = nullptr;  // [2][w_max]
     uint32_t *produced = nullptr;  // [2][w_max]
     uint32_t *log = nullptr;       // [log_epochs][w_max]
-    uint64_t *exch = nullptr;      // [2][max_tokens][exch_q]
+    uint64_t *exch = nullptr;      // [kExchPlanes][max_tokens][exch_q]
     uint64_t *place = nullptr;     // [2][w_max] XCD tags of each chunk's consumer / producer
     int exch_q = 1;                // exchange words per token and parity
     DevState *state = nullptr;
@@ -349,7 +349,7 @@ int sifar_init(const sifar_config *cfg, sifar_t *out) {
     if (!rc) rc = dev_alloc(&h->consumed, static_cast<size_t>(2) * h->w_max);
     if (!rc) rc = dev_alloc(&h->produced, static_cast<size_t>(2) * h->w_max);
     if (!rc) rc = dev_alloc(&h->log, static_cast<size_t>(c.log_epochs) * h->w_max);
-    if (!rc) rc = dev_alloc(&h->exch, static_cast<size_t>(2) * c.max_tokens * h->exch_q);
+    if (!rc) rc = dev_alloc(&h->exch, static_cast<size_t>(kExchPlanes) * c.max_tokens * h->exch_q);
     if (!rc) rc = dev_alloc(&h->place, static_cast<size_t>(2) * h->w_max);
     if (!rc) rc = dev_alloc(&h->state, 1);
     if (!rc && hipStreamCreateWithFlags(&h->capture, hipStreamNonBlocking) != hipSuccess)
@@ -366,7 +366,8 @@ int sifar_init(const sifar_config *cfg, sifar_t *out) {
             e = launch_fill_u32(h->log, 0, static_cast<uint64_t>(c.log_epochs) * h->w_max, s);
         if (e == hipSuccess)
             e = launch_fill_u32(reinterpret_cast<uint32_t *>(h->exch), 0,
-                                static_cast<uint64_t>(2) * c.max_tokens * h->exch_q * 2, s);
+                                static_cast<uint64_t>(kExchPlanes) * c.max_tokens * h->exch_q * 2,
+                                s);
         if (e == hipSuccess)
             e = launch_fill_u32(reinterpret_cast<uint32_t *>(h->place), 0,
                                 static_cast<uint64_t>(2) * h->w_max * 2, s);

@@ -422,6 +422,106 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
     residual_rmsnorm(a, k, g, o, rv, wv, a.y, lane, wave, G, blockIdx.x);
 }
 
+// The persistent step's epilogue in two halves, so that the wait for the
+// token's other groups overlaps the next epoch's reduction instead of
+// stalling every chunk of the token once per epoch. Only the residual carries
+// from one epoch to the next, and it is this chunk's own; the token-wide sum of
+// squares is needed for y alone. epi_stage runs right after epoch g's sum: it
+// updates the residual, reduces this group's sum of squares and publishes it
+// in exchange plane g mod kExchPlanes. epi_finish runs one epoch later, or
+// after the step's last epoch: it waits for the token's Q words of epoch g,
+// adds them in group order and writes y. The arithmetic and its order are
+// residual_rmsnorm's. Four planes suffice: a group can publish epoch g + 4
+// only after finishing epoch g + 2, which needs every group's word of g + 2,
+// and a group publishes that only after it finished epoch g.
+struct EpiPending {
+    float x[kVec];  // res' of this lane's 8 elements, widened to fp32
+    float grp;      // this workgroup's sum of squares
+    uint32_t g;     // the epoch
+};
+
+__device__ __forceinline__ void epi_stage(const ReduceArgs &a, const Chunk &k, uint32_t g,
+                                          const V16 &o, const V16 &rv, int lane, int wave, int G,
+                                          int q, bool xlocal, EpiPending &pd) {
+    V16 nr;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float a0 = lo_f32(o.w[i]), a1 = hi_f32(o.w[i]);
+        nr.w[i] = pack_bf16(a0 + lo_f32(rv.w[i]), a1 + hi_f32(rv.w[i]));
+        pd.x[2 * i] = lo_f32(nr.w[i]);
+        pd.x[2 * i + 1] = hi_f32(nr.w[i]);
+    }
+    if (k.lane_ok) st16(a.residual + k.row, nr);
+
+    float ss = 0.f;
+    if (k.lane_ok) {
+#pragma unroll
+        for (int i = 0; i < kVec; ++i) ss = __builtin_fmaf(pd.x[i], pd.x[i], ss);
+    }
+#pragma unroll
+    for (int off = kLanes / 2; off >= 1; off >>= 1) ss = ss + __shfl_xor(ss, off);
+
+    __shared__ float part[kMaxWavesPerGroup];
+    if (lane == 0) part[wave] = ss;
+    __syncthreads();
+    float grp = 0.f;
+    for (int w = 0; w < G; ++w) grp = grp + part[w];
+    pd.grp = grp;
+    pd.g = g;
+
+    const int Q = a.groups_per_token;
+    if (Q > 1 && wave == 0 && lane == 0) {
+        uint64_t *ex = a.exch + static_cast<size_t>(g % kExchPlanes) * a.exch_parity_stride +
+                       static_cast<size_t>(k.t) * Q;
+        const uint64_t word = (static_cast<uint64_t>(g) << 32) | __float_as_uint(grp);
+        // all groups of the token on this XCD: the word meets them in its L2
+        if (xlocal)
+            __hip_atomic_store(ex + q, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        else
+            __hip_atomic_store(ex + q, word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// `y` is the ring entry of epoch pd.g. (`pd` by value: with a reference the
+// compiler kept the pending state in scratch memory.)
+__device__ __forceinline__ void epi_finish(const ReduceArgs &a, const Chunk &k,
+                                           const EpiPending pd, const V16 &wv, uint16_t *y,
+                                           int lane, int wave) {
+    const int Q = a.groups_per_token;
+    float tot = pd.grp;
+    if (Q > 1) {
+        __shared__ float total;
+        if (wave == 0) {
+            const uint64_t *ex = a.exch +
+                                 static_cast<size_t>(pd.g % kExchPlanes) * a.exch_parity_stride +
+                                 static_cast<size_t>(k.t) * Q;
+            uint64_t mine = 0;
+            uint32_t spins = 0;
+            bool ready;
+            do {
+                if (lane < Q)
+                    mine = __hip_atomic_load(ex + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                ready = __ballot(lane < Q && static_cast<uint32_t>(mine >> 32) != pd.g) == 0;
+            } while (!ready && ++spins < a.spin_limit);
+            if (!ready && lane == 0) latch(a.err, kErrExchange, pd.g, k.c, spins);
+            const float pv = __uint_as_float(static_cast<uint32_t>(mine));
+            float sum = 0.f;
+            for (int j = 0; j < Q; ++j) sum = sum + __shfl(pv, j);
+            if (lane == 0) total = sum;
+        }
+        __syncthreads();
+        tot = total;
+    }
+    const float inv = 1.0f / __builtin_sqrtf(tot / static_cast<float>(a.geo.hidden) + a.eps);
+    V16 yo;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float w0 = lo_f32(wv.w[i]), w1 = hi_f32(wv.w[i]);
+        yo.w[i] = pack_bf16((pd.x[2 * i] * inv) * w0, (pd.x[2 * i + 1] * inv) * w1);
+    }
+    if (k.lane_ok) st16(y + k.row, yo);
+}
+
 // ---------------------------------------------------------------------------
 // Persistent decode step: one launch runs all L all-reduces. All waves are
 // co-resident (the host checks), and every wait is bounded.
@@ -569,6 +669,8 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
     }
     V16 wv;
     if (EPI) wv = ld16(a.weight + k.elem);
+    EpiPending pending;   // the epilogue of the previous epoch, finished one epoch late
+    bool have_pending = false;
     const uint32_t *stamps = a.stamps + static_cast<size_t>(k.c) * N + lane;
     const size_t parity_stride = static_cast<size_t>(geo.w_max) * N;
     for (int i = 0; i < A.reduces; ++i) {
@@ -602,15 +704,23 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
         if (!EPI) {
             if (k.lane_ok) st16(a.out + ring + k.row, o);
         } else {
-            residual_rmsnorm(a, k, g, o, rv, wv, a.y + ring, lane, wave, G, bx, xlocal);
+            EpiPending cur;
+            epi_stage(a, k, g, o, rv, lane, wave, G, bx, xlocal, cur);
+            if (have_pending) epi_finish(a, k, pending, wv, a.y + ring - A.ring_stride, lane, wave);
+            pending = cur;
+            have_pending = true;
         }
-        // a bounded wait failed somewhere: stop the step
+        // a bounded wait failed somewhere: stop the step (a pending epilogue
+        // stays unwritten: the step has failed)
         if (GROUPED && EPI) {
             if (__syncthreads_or(err_seen != 0)) return;
         } else if (err_seen != 0) {
             return;
         }
     }
+    if (EPI && have_pending)
+        epi_finish(a, k, pending, wv, a.y + static_cast<uint64_t>(A.reduces - 1) * A.ring_stride,
+                   lane, wave);
 }
 
 // Grid (segs / G, tokens, 2) of G-wave workgroups (G = 1, or kChainGroupWaves

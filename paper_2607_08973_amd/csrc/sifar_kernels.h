@@ -13,6 +13,7 @@ constexpr int kChunk = kLanes * kVec;      // elements per chunk: one wave, one 
 constexpr int kMaxRanks = 8;
 constexpr int kMaxWavesPerGroup = 16;
 constexpr int kChainGroupWaves = 4;         // waves per persistent-step workgroup when grouped
+constexpr int kExchPlanes = 4;              // epoch-indexed planes of the epilogue exchange
 
 // Device-resident state shared by all kernels of a handle.
 struct DevState {
@@ -74,7 +75,9 @@ struct ReduceArgs {
     uint16_t *residual;          // epilogue: [tokens][hidden], in place
     const uint16_t *weight;      // [hidden]
     uint16_t *y;                 // [tokens][hidden]
-    uint64_t *exch;              // [2][max_tokens][groups_per_token]: (epoch << 32) | partial bits
+    uint64_t *exch;              // [kExchPlanes][max_tokens][groups_per_token]: (epoch << 32) |
+                                 // partial bits; per-launch epilogues use planes g & 1,
+                                 // persistent steps g mod kExchPlanes
     int32_t groups_per_token;
     int32_t exch_parity_stride;  // max_tokens * groups_per_token
     float eps;
