@@ -459,6 +459,25 @@ def test_persistent_many_steps_sampled():
     run.s.close()
 
 
+@pytest.mark.parametrize("persistent", [0, 1])
+def test_steps_with_a_changing_batch_size(persistent):
+    """Decode steps whose token count changes from step to step (seeded draws
+    from 1..8), so chunks sit idle for some steps and are picked up again with
+    older stamps and slot words; every output of every step is checked."""
+    w = synth.LLAMA8B_DECODE
+    run = StepRun(w, 8, persistent=persistent)
+    rng = np.random.default_rng(4242)
+    for step in range(24):
+        T = int(rng.integers(1, 9))
+        epochs = run.step(T)
+        got = to_host(run.out_d)
+        for i, g in enumerate(epochs):
+            exp = oracle.reduce(run.pool[(g - 1) % run.pool.shape[0]][:, :T])
+            assert np.array_equal(got[i, :T], exp), f"step {step} T={T} node {i}"
+    run.s.check()
+    run.s.close()
+
+
 @pytest.mark.parametrize("T", [4, 8])
 def test_persistent_late_stamps(T):
     """Late ranks' stamps land after a delay while the reduction waits on them:
