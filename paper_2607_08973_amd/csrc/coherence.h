@@ -41,23 +41,41 @@ constexpr int32_t kBufferWord3 = 0x00020000;
 // Cache policy of a buffer load: SC1 set, SC0 clear = agent scope.
 constexpr int32_t kCachePolicyAgent = 16;
 
+// Buffer descriptor of `base` (the same in every lane of the wave).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(uniform_ptr(base)), 0, 0x7fffffff,
+                                             kBufferWord3);
+}
+
+typedef int V4i __attribute__((ext_vector_type(4)));
+
 // 16 bytes at byte offset `off` (per lane, below 2^31) from `base` (the same
-// in every lane of the wave) with the agent-scope cache policy: the load
-// bypasses this CU's L1 and is served by the XCD's L2 or memory -- the caching
-// of an agent-scope atomic load, in one 16-byte load instead of two 8-byte
-// ones.
-__device__ __forceinline__ V16 ld16_agent(const void *base, uint32_t off) {
-    typedef int v4i __attribute__((ext_vector_type(4)));
-    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<void *>(uniform_ptr(base)), 0, 0x7fffffff, kBufferWord3);
-    const v4i x = __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0,
-                                                        kCachePolicyAgent);
+// in every lane of the wave) through a buffer descriptor: the address lives in
+// scalar registers and the only vector register the access reads is `off`.
+// POLICY 0 caches normally; kCachePolicyAgent bypasses this CU's L1 (the
+// caching of an agent-scope atomic load, in one 16-byte load instead of two
+// 8-byte ones) and is served by the XCD's L2 or memory.
+template <int POLICY>
+__device__ __forceinline__ V16 ld16_buffer(const void *base, uint32_t off) {
+    const V4i x = __builtin_amdgcn_raw_buffer_load_b128(buffer_rsrc(base), static_cast<int>(off),
+                                                        0, POLICY);
     V16 v;
     v.w[0] = static_cast<uint32_t>(x[0]);
     v.w[1] = static_cast<uint32_t>(x[1]);
     v.w[2] = static_cast<uint32_t>(x[2]);
     v.w[3] = static_cast<uint32_t>(x[3]);
     return v;
+}
+
+__device__ __forceinline__ V16 ld16_agent(const void *base, uint32_t off) {
+    return ld16_buffer<kCachePolicyAgent>(base, off);
+}
+
+// The store counterpart of ld16_buffer (normal caching).
+__device__ __forceinline__ void st16_buffer(void *base, uint32_t off, const V16 &v) {
+    const V4i x = {static_cast<int>(v.w[0]), static_cast<int>(v.w[1]), static_cast<int>(v.w[2]),
+                   static_cast<int>(v.w[3])};
+    __builtin_amdgcn_raw_buffer_store_b128(x, buffer_rsrc(base), static_cast<int>(off), 0, 0);
 }
 
 __device__ __forceinline__ void st16(uint16_t *p, const V16 &v) {
@@ -149,6 +167,12 @@ __device__ __forceinline__ bool tag_is_local(const uint64_t *place, uint32_t bas
     }
     return t == want;
 }
+
+// s_waitcnt immediate (gfx9 family: vmcnt in bits 3:0 and 15:14, expcnt 6:4,
+// lgkmcnt 11:8) with the export and LDS/scalar counts at their maxima and the
+// vector-memory count 0; OR in n < 16 to wait until at most n vector memory
+// operations of the wave are outstanding.
+constexpr int kWaitVm = 0x0F70;
 
 // Publication of a producer's slot stores before its stamps. To a consumer on
 // another XCD: an agent-scope release fence, which writes back this XCD's L2.

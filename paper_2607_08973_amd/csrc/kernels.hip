@@ -43,11 +43,13 @@ namespace {
 __device__ __forceinline__ float lo_f32(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float hi_f32(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
+// Two fp32 values to two bf16 in one V_CVT_PK_BF16_F32 (round to nearest
+// even); converting them one at a time costs four instructions per pair.
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
-    const __bf16 a = static_cast<__bf16>(lo);
-    const __bf16 b = static_cast<__bf16>(hi);
-    return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
-           (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    const f32x2 f = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
 }
 
 __device__ __forceinline__ uint32_t epoch_of(const EpochRef &e) { return e.base[0] + e.off; }
@@ -68,8 +70,10 @@ __device__ __forceinline__ bool latched(const uint32_t *err) { return ld_relaxed
 constexpr uint32_t kErrRetryBudget = 1, kErrWaw = 2, kErrExchange = 3;
 
 // Where the calling lane works: token t, chunk s of the row, chunk index c.
-// Lanes past the end of the row load a clamped, in-bounds address and do not
-// store (lane_ok false); waves past the last chunk are inactive.
+// Lanes past the end of the row load a clamped, in-bounds address (the row's
+// last 8 elements) and do not store (lane_ok false) -- except where a store of
+// the very bytes the owning lane stores keeps a loop branch-free; waves past
+// the last chunk are inactive.
 struct Chunk {
     int t, s, c;
     bool active, lane_ok;
@@ -99,7 +103,45 @@ __device__ __forceinline__ uint32_t log_word(uint32_t attempts, uint32_t first, 
 // ---------------------------------------------------------------------------
 // Producer side: the emulated peers.
 
-// Copy every rank's part of chunk k of epoch g into the slots of parity p.
+// Index of chunk k's first element in a row-major [tokens][hidden] array
+// (wave-uniform), and the calling lane's byte offset from it.
+__device__ __forceinline__ uint64_t chunk_first(const Geometry &geo, const Chunk &k) {
+    return static_cast<uint64_t>(k.t) * geo.hidden + static_cast<uint64_t>(k.s) * kChunk;
+}
+
+__device__ __forceinline__ uint32_t lane_offset(const Geometry &geo, const Chunk &k) {
+    return static_cast<uint32_t>(k.row - chunk_first(geo, k)) * 2u;
+}
+
+// Every rank's part of chunk k of epoch g (the peers' partial results), read
+// through buffer descriptors: the per-lane address is the loop-invariant
+// offset, so no vector register of an access in flight is ever rewritten.
+template <int N>
+__device__ __forceinline__ void load_sources(const ProduceArgs &a, const Chunk &k, uint32_t g,
+                                             V16 (&v)[N]) {
+    const uint32_t e = (g - 1u) % static_cast<uint32_t>(a.entries);
+    const uint16_t *src = a.src + e * a.entry_stride + static_cast<int64_t>(chunk_first(a.geo, k));
+    const uint32_t off = lane_offset(a.geo, k);
+#pragma unroll
+    for (int r = 0; r < N; ++r) v[r] = ld16_buffer<0>(src + r * a.rank_stride, off);
+}
+
+// ... written into the slots of parity p.
+template <int N>
+__device__ __forceinline__ void store_slots(const ProduceArgs &a, const Chunk &k, uint32_t p,
+                                            const V16 (&v)[N]) {
+    const Geometry &geo = a.geo;
+    uint16_t *dst = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + chunk_first(geo, k);
+    const uint32_t off = lane_offset(geo, k);
+    if (k.lane_ok) {
+#pragma unroll
+        for (int r = 0; r < N; ++r) st16_buffer(dst + r * 2 * geo.slot_elems, off, v[r]);
+    }
+}
+
+// Copy every rank's part of chunk k of epoch g into the slots of parity p
+// (the producers that load and store in one go; plain global addressing
+// measured faster for them than the buffer form above).
 template <int N>
 __device__ __forceinline__ void copy_chunk(const ProduceArgs &a, const Chunk &k, uint32_t g,
                                            uint32_t p) {
@@ -228,27 +270,25 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
 }
 
 // Persistent-step gather of an active chunk: a producer may be writing right
-// now, so only ORDERED is sound. `st` holds this lane's first stamp poll
-// (issued by the caller); polls repeat (relaxed agent-scope loads, short
-// sleeps) until every stamp is fresh, then the payload is loaded -- after an
-// acquire fence when the producer is on another XCD, directly when it shares
-// this XCD (see publish_slot).
+// now, so only ORDERED is sound. `m` is the stale-rank mask of the first stamp
+// poll (issued and evaluated by the caller); polls repeat (relaxed agent-scope
+// loads, short sleeps) until every stamp is fresh, then the payload is loaded
+// -- after an acquire fence when the producer is on another XCD, directly when
+// it shares this XCD (see publish_slot).
 template <int N>
 __device__ __forceinline__ void gather_chain(const ReduceArgs &a, const Chunk &k, uint32_t g,
-                                             uint32_t p, int lane, uint32_t st, V16 (&v)[N],
+                                             uint32_t p, int lane, uint32_t m, V16 (&v)[N],
                                              uint32_t &attempts, uint32_t &first,
                                              uint32_t &last, bool local) {
     const Geometry &geo = a.geo;
     // the chunk's first element in rank 0's slot (wave-uniform) and this
     // lane's byte offset from it
-    const uint64_t row0 = static_cast<uint64_t>(k.t) * geo.hidden +
-                          static_cast<uint64_t>(k.s) * kChunk;
-    const uint16_t *chunk0 = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + row0;
-    const uint32_t off = static_cast<uint32_t>(k.row - row0) * 2u;
+    const uint16_t *chunk0 =
+        a.slots + static_cast<uint64_t>(p) * geo.slot_elems + chunk_first(geo, k);
+    const uint32_t off = lane_offset(geo, k);
     const uint64_t rank_step = 2 * geo.slot_elems;  // slots are [rank][parity]
     const uint32_t *stamp = a.stamps + (static_cast<size_t>(p) * geo.w_max + k.c) * N;
     attempts = 1;
-    uint32_t m = static_cast<uint32_t>(__ballot(lane < N && st != g));
     first = last = m;
     bool fail = m != 0 || a.forced_retries >= 1;
     while (fail) {
@@ -256,14 +296,15 @@ __device__ __forceinline__ void gather_chain(const ReduceArgs &a, const Chunk &k
             if (lane == 0) latch(a.err, kErrRetryBudget, g, k.c, attempts);
             break;
         }
-        if (m != 0) {
-            if (latched(a.err)) break;  // the step is already failing: stop waiting
-            __builtin_amdgcn_s_sleep(1);
-        }
+        if (m != 0) __builtin_amdgcn_s_sleep(1);
+        // one round trip per poll: the stamps and the error word together
+        const uint32_t e = ld_relaxed(a.err);
+        uint32_t st = 0;
         if (lane < N) st = ld_relaxed(stamp + lane);
         ++attempts;
         m = static_cast<uint32_t>(__ballot(lane < N && st != g));
         last = m;
+        if (m != 0 && e != 0) break;  // the step is already failing: stop waiting
         fail = m != 0 || attempts <= a.forced_retries;
     }
     acquire_slot(local);
@@ -546,10 +587,11 @@ __device__ __forceinline__ void epi_finish(const ReduceArgs &a, const Chunk &k,
 // The producer can run one epoch ahead of the consumer, no further.
 // Producer wave of chunk (t, s), one epoch after the other: wait until the
 // slot of this parity is free (with a single buffer: until the previous
-// epoch's reduction is done -- the bottom barrier), copy, publish, stamps.
-// (Measured on MI355X: prefetching the next epoch's sources or batching
-// several chunks per wave behind one fence does not shorten the step -- the
-// dual-buffer rule ties the producer of g + 1 to the reduction of g - 1.)
+// epoch's reduction is done -- the bottom barrier), store the sources already
+// in registers, publish, stamps. Loading the next epoch's sources while the
+// slot stores travel shortened the llama8b decode step by ~5 % on MI355X once
+// the consumer issued its polls ahead of its stores; before that the consumer
+// bounded the step and the prefetch made no difference.
 template <int N>
 __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base, int lane,
                                                int bx, int by) {
@@ -558,24 +600,40 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
     const Chunk k = chunk_at(geo, by, bx, lane);
     publish_place(A.place + geo.w_max + k.c, base, lane);
     const bool local = partner_is_local(A.place + k.c, base, lane);
-    for (int i = 0; i < A.reduces; ++i) {
+    // One epoch: wait until the slot is free, store `cur` (the epoch's
+    // sources, already in registers), load the next epoch's sources into
+    // `nxt` while the slot stores travel (harmless in-bounds reads after the
+    // last epoch), publish, stamp. False when the slot wait failed.
+    auto epoch = [&](int i, const V16(&cur)[N], V16(&nxt)[N]) -> bool {
         const uint32_t g = base + static_cast<uint32_t>(i) + 1u;
         const uint32_t p = static_cast<uint32_t>(i + 1) & A.parity_mask;
         const size_t pc = static_cast<size_t>(p) * geo.w_max + k.c;
         uint32_t spins = 0;
         bool free = false;
-        while (true) {
-            free = ld_relaxed(a.consumed + pc) == ld_relaxed(a.produced + pc);
-            if (free || ++spins >= A.r.spin_limit || latched(a.err)) break;
+        while (true) {  // one round trip per poll: both words and the error word together
+            const uint32_t done = ld_relaxed(a.consumed + pc);
+            const uint32_t prev = ld_relaxed(a.produced + pc);
+            const uint32_t e = ld_relaxed(a.err);
+            free = done == prev;
+            if (free || ++spins >= A.r.spin_limit || e != 0) break;
             __builtin_amdgcn_s_sleep(1);
         }
         if (!free) {
             if (lane == 0) latch(a.err, kErrWaw, g, k.c, spins);
-            return;
+            return false;
         }
-        copy_chunk<N>(a, k, g, p);
         const uint32_t held = held_back(a.inject, a.inject_entries, g);
-        publish_slot(local);
+        store_slots<N>(a, k, p, cur);
+        load_sources<N>(a, k, g + 1u, nxt);
+        if (local) {
+            // Loads and stores complete in issue order on gfx9-family GPUs:
+            // with at most N operations outstanding the slot stores have
+            // reached the L2 and only the N source loads are still in flight.
+            __builtin_amdgcn_s_waitcnt(kWaitVm | N);
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        } else {
+            publish_slot(false);
+        }
         uint32_t *stamp = a.stamps + pc * N;
         if (lane < N && !((held >> lane) & 1u)) st_flag(stamp + lane, g, local);
         if (lane == 0) st_flag(a.produced + pc, g, local);
@@ -585,6 +643,16 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
             if (lane < N && ((inj >> lane) & 1u) && !((inj >> (8 + lane)) & 1u))
                 st_flag(stamp + lane, g, local);
         }
+        return true;
+    };
+    // Two register sets taking turns: a load never overwrites the data of a
+    // store still in flight, so nothing waits for the store acknowledgements
+    // before the next sources are requested.
+    V16 va[N], vb[N];
+    load_sources<N>(a, k, base + 1u, va);
+    for (int i = 0; i < A.reduces; i += 2) {
+        if (!epoch(i, va, vb)) return;
+        if (i + 1 < A.reduces && !epoch(i + 1, vb, va)) return;
     }
 }
 
@@ -616,9 +684,12 @@ __device__ __forceinline__ void chain_producer_grouped(const ChainArgs &A, uint3
         if (k.active) {
             const size_t pc = static_cast<size_t>(p) * geo.w_max + k.c;
             uint32_t spins = 0;
-            while (true) {
-                free = ld_relaxed(a.consumed + pc) == ld_relaxed(a.produced + pc);
-                if (free || ++spins >= A.r.spin_limit || latched(a.err)) break;
+            while (true) {  // one round trip per poll, as in chain_producer
+                const uint32_t done = ld_relaxed(a.consumed + pc);
+                const uint32_t prev = ld_relaxed(a.produced + pc);
+                const uint32_t e = ld_relaxed(a.err);
+                free = done == prev;
+                if (free || ++spins >= A.r.spin_limit || e != 0) break;
                 __builtin_amdgcn_s_sleep(1);
             }
             if (!free && lane == 0) latch(a.err, kErrWaw, g, k.c, spins);
@@ -671,38 +742,65 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
     if (EPI) wv = ld16(a.weight + k.elem);
     EpiPending pending;   // the epilogue of the previous epoch, finished one epoch late
     bool have_pending = false;
-    const uint32_t *stamps = a.stamps + static_cast<size_t>(k.c) * N + lane;
+    // Every lane polls a stamp of this chunk (lanes >= N repeat rank N - 1's,
+    // which the ballot ignores), so no branch surrounds the poll.
+    const uint32_t *stamps = a.stamps + static_cast<size_t>(k.c) * N + (lane < N ? lane : N - 1);
     const size_t parity_stride = static_cast<size_t>(geo.w_max) * N;
+    // The first poll of an epoch -- its stamps and the error word -- is issued
+    // before the previous epoch's stores. On gfx9-family GPUs one counter
+    // (vmcnt) tracks loads and stores in issue order, so a poll issued after
+    // the stores could only be waited for together with their write
+    // acknowledgements. The stores below are therefore branch-free too, so the
+    // compiler can count them and wait for the poll alone. An early poll that
+    // reads stale is repeated; the payload is still loaded only after fresh
+    // stamps were seen.
+    uint32_t err_word = ld_relaxed(a.err);
+    uint32_t st_next = ld_relaxed(stamps + (1u & A.parity_mask) * parity_stride);
+    // stale ranks of the first poll, evaluated where the wait for it is exact
+    uint32_t m_next = static_cast<uint32_t>(__ballot(lane < N && st_next != base + 1u));
     for (int i = 0; i < A.reduces; ++i) {
         const uint32_t g = base + static_cast<uint32_t>(i) + 1u;
         const uint32_t p = static_cast<uint32_t>(i + 1) & A.parity_mask;
-        // read now, acted on after the payload: waiting for the payload covers it
-        const uint32_t err_seen = ld_relaxed(a.err);
         V16 rv;
         if (EPI) rv = ld16(a.residual + k.row);  // this wave's own previous store
         V16 v[N];
         uint32_t attempts, first, last;
-        uint32_t st = 0;
-        if (lane < N) st = ld_relaxed(stamps + p * parity_stride);
-        gather_chain<N>(a, k, g, p, lane, st, v, attempts, first, last, local);
+        gather_chain<N>(a, k, g, p, lane, m_next, v, attempts, first, last, local);
         uint32_t *consumed = a.consumed + static_cast<size_t>(p) * geo.w_max + k.c;
+        bool stop = false;
+        // Once the payload has arrived: note the error word read with this
+        // epoch's first poll (loads return in order, so it has arrived too),
+        // issue the next epoch's first polls (harmless in-bounds reads after
+        // the last epoch), then release the slot (every lane stores the same
+        // word).
+        auto poll_next_and_release = [&]() {
+            stop = err_word != 0;
+            const uint32_t pn = static_cast<uint32_t>(i + 2) & A.parity_mask;
+            err_word = ld_relaxed(a.err);
+            st_next = ld_relaxed(stamps + pn * parity_stride);
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);  // keep the polls ahead of the stores
+            st_flag(consumed, g, local);
+        };
         if (!EPI) {
             // release the slot as soon as every payload load has returned (the
             // sum works on registers); measured faster for the plain chain,
             // slower with the epilogue
 #pragma unroll
             for (int r = 0; r < N; ++r) complete(v[r]);
-            if (lane == 0) st_flag(consumed, g, local);
+            poll_next_and_release();
         }
         const V16 o = sum_round<N>(v);
         if (EPI) {
             complete(o);  // every payload load has returned before the slot is released
-            if (lane == 0) st_flag(consumed, g, local);
+            poll_next_and_release();
         }
-        if (lane == 0) write_log(a, k, g, log_word(attempts, first, last));
+        write_log(a, k, g, log_word(attempts, first, last));  // wave-uniform word
         const uint64_t ring = static_cast<uint64_t>(i) * A.ring_stride;
         if (!EPI) {
-            if (k.lane_ok) st16(a.out + ring + k.row, o);
+            // Lanes past the end of the row loaded the row's last 8 elements
+            // (clamped) with the same instruction as the lane that owns them,
+            // so they store the same bytes to the same place: no branch.
+            st16(a.out + ring + k.row, o);
         } else {
             EpiPending cur;
             epi_stage(a, k, g, o, rv, lane, wave, G, bx, xlocal, cur);
@@ -710,11 +808,14 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
             pending = cur;
             have_pending = true;
         }
+        // The next epoch's first poll, after this epoch's stores: the
+        // compiler waits for the poll alone and leaves the stores in flight.
+        m_next = static_cast<uint32_t>(__ballot(lane < N && st_next != g + 1u));
         // a bounded wait failed somewhere: stop the step (a pending epilogue
         // stays unwritten: the step has failed)
         if (GROUPED && EPI) {
-            if (__syncthreads_or(err_seen != 0)) return;
-        } else if (err_seen != 0) {
+            if (__syncthreads_or(stop)) return;
+        } else if (stop) {
             return;
         }
     }
