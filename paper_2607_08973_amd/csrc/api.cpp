@@ -19,6 +19,7 @@ struct sifar_ctx {
     int w_max = 0;         // max_tokens * segs
     int groups_per_token = 1;
     bool chain_grouping = false;  // persistent steps may use kChainGroupWaves-wave workgroups
+    bool chain_prefetch = false;  // one-wave persistent steps' producers load sources ahead
     uint64_t slot_elems = 0;
 
     uint16_t *slots = nullptr;     // [N][2][slot_elems]
@@ -333,13 +334,19 @@ int sifar_init(const sifar_config *cfg, sifar_t *out) {
         const int64_t tokens = c.epilogue ? 8 * ((static_cast<int64_t>(c.max_tokens) + 7) / 8)
                                           : c.max_tokens;
         const int64_t waves = 2 * tokens * h->segs;
-        const int cap = max_active_chain_groups(c.nranks, c.validate, c.epilogue != 0, 1);
+        // the prefetching producer holds two epochs' sources: it needs more
+        // registers, so it runs wherever the step still fits with them
+        const int pcap = max_active_chain_groups(c.nranks, c.validate, c.epilogue != 0, 1, true);
+        h->chain_prefetch = pcap > 0 && waves <= pcap;
+        const int cap = h->chain_prefetch
+                            ? pcap
+                            : max_active_chain_groups(c.nranks, c.validate, c.epilogue != 0, 1, false);
         if (cap <= 0 || waves > cap) {
             delete h;
             return SIFAR_EINVAL;
         }
         const int gcap = max_active_chain_groups(c.nranks, c.validate, c.epilogue != 0,
-                                                 kChainGroupWaves);
+                                                 kChainGroupWaves, false);
         h->chain_grouping = c.nranks * kChainGroupWaves <= kLanes && gcap > 0 &&
                             waves / kChainGroupWaves <= gcap;
     }
@@ -503,7 +510,8 @@ int sifar_step(sifar_t h, int32_t tokens, void *stream) {
         }
         ChainArgs ca{};
         const int waves = chain_args(h, tokens, &ca);
-        rc = hip_status(launch_chain(ca, h->cfg.validate, h->cfg.epilogue != 0, waves, s));
+        rc = hip_status(
+            launch_chain(ca, h->cfg.validate, h->cfg.epilogue != 0, waves, h->chain_prefetch, s));
         if (rc) return rc;
         h->base_host = base + static_cast<uint32_t>(L + (L & 1));
         h->next_prod = h->next_red = base + static_cast<uint32_t>(L) + 1;

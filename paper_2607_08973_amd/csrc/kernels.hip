@@ -592,7 +592,7 @@ __device__ __forceinline__ void epi_finish(const ReduceArgs &a, const Chunk &k,
 // slot stores travel shortened the llama8b decode step by ~5 % on MI355X once
 // the consumer issued its polls ahead of its stores; before that the consumer
 // bounded the step and the prefetch made no difference.
-template <int N>
+template <int N, bool PREFETCH>
 __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base, int lane,
                                                int bx, int by) {
     const ProduceArgs &a = A.p;
@@ -623,15 +623,20 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
             return false;
         }
         const uint32_t held = held_back(a.inject, a.inject_entries, g);
-        store_slots<N>(a, k, p, cur);
-        load_sources<N>(a, k, g + 1u, nxt);
-        if (local) {
+        if (!PREFETCH) {
+            copy_chunk<N>(a, k, g, p);
+            publish_slot(local);
+        } else if (local) {
+            store_slots<N>(a, k, p, cur);
+            load_sources<N>(a, k, g + 1u, nxt);
             // Loads and stores complete in issue order on gfx9-family GPUs:
             // with at most N operations outstanding the slot stores have
             // reached the L2 and only the N source loads are still in flight.
             __builtin_amdgcn_s_waitcnt(kWaitVm | N);
             __atomic_signal_fence(__ATOMIC_SEQ_CST);
         } else {
+            store_slots<N>(a, k, p, cur);
+            load_sources<N>(a, k, g + 1u, nxt);
             publish_slot(false);
         }
         uint32_t *stamp = a.stamps + pc * N;
@@ -647,9 +652,11 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
     };
     // Two register sets taking turns: a load never overwrites the data of a
     // store still in flight, so nothing waits for the store acknowledgements
-    // before the next sources are requested.
+    // before the next sources are requested. (Without PREFETCH every epoch
+    // loads and stores in one go: 2N fewer registers, for steps whose waves
+    // fit on the GPU only at the higher occupancy.)
     V16 va[N], vb[N];
-    load_sources<N>(a, k, base + 1u, va);
+    if (PREFETCH) load_sources<N>(a, k, base + 1u, va);
     for (int i = 0; i < A.reduces; i += 2) {
         if (!epoch(i, va, vb)) return;
         if (i + 1 < A.reduces && !epoch(i + 1, vb, va)) return;
@@ -830,7 +837,7 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
 // base+1 .. base+L in order, plane 1 produces it. The last wave to arrive on
 // the counter advances the epoch base for the next step: every wave read the
 // base before it arrived, so no wave can see the advanced value.
-template <int N, int MODE, bool EPI, bool GROUPED>
+template <int N, int MODE, bool EPI, bool GROUPED, bool PREFETCH>
 __global__ __launch_bounds__(GROUPED ? kChainGroupWaves * kLanes : kLanes) void chain_kernel(
     ChainArgs A) {
     const int lane = threadIdx.x & (kLanes - 1);
@@ -855,7 +862,7 @@ __global__ __launch_bounds__(GROUPED ? kChainGroupWaves * kLanes : kLanes) void 
             if (GROUPED)
                 chain_producer_grouped<N>(A, base, lane, wave, G, bx, by);
             else
-                chain_producer<N>(A, base, lane, bx, by);
+                chain_producer<N, PREFETCH>(A, base, lane, bx, by);
         } else {
             chain_consumer<N, MODE, EPI, GROUPED>(A, base, lane, wave, G, bx, by);
         }
@@ -915,31 +922,35 @@ hipError_t launch_reduce_n(const ReduceArgs &a, const ProduceArgs *pa, int mode,
     return hipErrorInvalidValue;
 }
 
+// The grouped producer loads and stores in one go; with the epilogue the
+// consumer sets the register count, so only the plain one-wave-per-chunk
+// kernel comes in both producer forms.
 template <int N, int MODE>
-const void *chain_fn(bool epi, bool grouped) {
+const void *chain_fn(bool epi, bool grouped, bool prefetch) {
     if (grouped)
-        return epi ? reinterpret_cast<const void *>(chain_kernel<N, MODE, true, true>)
-                   : reinterpret_cast<const void *>(chain_kernel<N, MODE, false, true>);
-    return epi ? reinterpret_cast<const void *>(chain_kernel<N, MODE, true, false>)
-               : reinterpret_cast<const void *>(chain_kernel<N, MODE, false, false>);
+        return epi ? reinterpret_cast<const void *>(chain_kernel<N, MODE, true, true, false>)
+                   : reinterpret_cast<const void *>(chain_kernel<N, MODE, false, true, false>);
+    if (epi) return reinterpret_cast<const void *>(chain_kernel<N, MODE, true, false, true>);
+    return prefetch ? reinterpret_cast<const void *>(chain_kernel<N, MODE, false, false, true>)
+                    : reinterpret_cast<const void *>(chain_kernel<N, MODE, false, false, false>);
 }
 
 // Persistent steps validate before they load: ORDERED only.
 template <int N>
-const void *chain_fn_n(int mode, bool epi, bool grouped) {
-    return mode == kOrdered ? chain_fn<N, kOrdered>(epi, grouped) : nullptr;
+const void *chain_fn_n(int mode, bool epi, bool grouped, bool prefetch) {
+    return mode == kOrdered ? chain_fn<N, kOrdered>(epi, grouped, prefetch) : nullptr;
 }
 
-const void *chain_fn_any(int nranks, int mode, bool epi, bool grouped) {
+const void *chain_fn_any(int nranks, int mode, bool epi, bool grouped, bool prefetch) {
     switch (nranks) {
-        case 1: return chain_fn_n<1>(mode, epi, grouped);
-        case 2: return chain_fn_n<2>(mode, epi, grouped);
-        case 3: return chain_fn_n<3>(mode, epi, grouped);
-        case 4: return chain_fn_n<4>(mode, epi, grouped);
-        case 5: return chain_fn_n<5>(mode, epi, grouped);
-        case 6: return chain_fn_n<6>(mode, epi, grouped);
-        case 7: return chain_fn_n<7>(mode, epi, grouped);
-        case 8: return chain_fn_n<8>(mode, epi, grouped);
+        case 1: return chain_fn_n<1>(mode, epi, grouped, prefetch);
+        case 2: return chain_fn_n<2>(mode, epi, grouped, prefetch);
+        case 3: return chain_fn_n<3>(mode, epi, grouped, prefetch);
+        case 4: return chain_fn_n<4>(mode, epi, grouped, prefetch);
+        case 5: return chain_fn_n<5>(mode, epi, grouped, prefetch);
+        case 6: return chain_fn_n<6>(mode, epi, grouped, prefetch);
+        case 7: return chain_fn_n<7>(mode, epi, grouped, prefetch);
+        case 8: return chain_fn_n<8>(mode, epi, grouped, prefetch);
     }
     return nullptr;
 }
@@ -1026,9 +1037,10 @@ hipError_t launch_reduce(const ReduceArgs &a, const ProduceArgs *next, int mode,
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_chain(const ChainArgs &a, int mode, bool epilogue, int waves, hipStream_t s) {
+hipError_t launch_chain(const ChainArgs &a, int mode, bool epilogue, int waves, bool prefetch,
+                        hipStream_t s) {
     if (waves != 1 && waves != kChainGroupWaves) return hipErrorInvalidValue;
-    const void *fn = chain_fn_any(a.r.geo.nranks, mode, epilogue, waves > 1);
+    const void *fn = chain_fn_any(a.r.geo.nranks, mode, epilogue, waves > 1, prefetch);
     if (!fn) return hipErrorInvalidValue;
     if (a.r.geo.segs != a.p.geo.segs || a.r.geo.tokens != a.p.geo.tokens ||
         a.r.geo.segs % waves != 0 || (waves > 1 && waves * a.r.geo.nranks > kLanes))
@@ -1046,9 +1058,10 @@ int max_active_groups(int nranks, int mode, bool epilogue, int waves_per_group) 
     return resident_groups(reduce_fn_any(nranks, mode, epilogue), waves_per_group * kLanes);
 }
 
-int max_active_chain_groups(int nranks, int mode, bool epilogue, int waves) {
+int max_active_chain_groups(int nranks, int mode, bool epilogue, int waves, bool prefetch) {
     if (waves != 1 && waves != kChainGroupWaves) return 0;
-    return resident_groups(chain_fn_any(nranks, mode, epilogue, waves > 1), waves * kLanes);
+    return resident_groups(chain_fn_any(nranks, mode, epilogue, waves > 1, prefetch),
+                           waves * kLanes);
 }
 
 hipError_t launch_advance(uint32_t *epoch_base, uint32_t step, hipStream_t s) {

@@ -111,12 +111,14 @@ hipError_t launch_reduce(const ReduceArgs &a, const ProduceArgs *next, int mode,
 // current device (0 if unknown).
 int max_active_groups(int nranks, int mode, bool epilogue, int waves_per_group);
 // Same for the persistent chain kernel's workgroups of `waves` waves (1 or
-// kChainGroupWaves).
-int max_active_chain_groups(int nranks, int mode, bool epilogue, int waves);
+// kChainGroupWaves); `prefetch` picks the one-wave kernel whose producer loads
+// an epoch's sources ahead (more registers, lower occupancy).
+int max_active_chain_groups(int nranks, int mode, bool epilogue, int waves, bool prefetch);
 // Persistent step: grid (segs / waves, tokens, 2); waves = 1, or
 // kChainGroupWaves (segs divisible by it, waves * nranks <= 64) to let one
 // release fence cover a workgroup's chunks.
-hipError_t launch_chain(const ChainArgs &a, int mode, bool epilogue, int waves, hipStream_t s);
+hipError_t launch_chain(const ChainArgs &a, int mode, bool epilogue, int waves, bool prefetch,
+                        hipStream_t s);
 hipError_t launch_advance(uint32_t *epoch_base, uint32_t step, hipStream_t s);
 hipError_t launch_set_base(uint32_t *epoch_base, uint32_t value, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t *p, uint32_t value, uint64_t count, hipStream_t s);
