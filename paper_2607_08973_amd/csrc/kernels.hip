@@ -272,7 +272,7 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
 // Persistent-step gather of an active chunk: a producer may be writing right
 // now, so only ORDERED is sound. `m` is the stale-rank mask of the first stamp
 // poll (issued and evaluated by the caller); polls repeat (relaxed agent-scope
-// loads, short sleeps) until every stamp is fresh, then the payload is loaded
+// loads) until every stamp is fresh, then the payload is loaded
 // -- after an acquire fence when the producer is on another XCD, directly when
 // it shares this XCD (see publish_slot).
 template <int N>
@@ -296,8 +296,8 @@ __device__ __forceinline__ void gather_chain(const ReduceArgs &a, const Chunk &k
             if (lane == 0) latch(a.err, kErrRetryBudget, g, k.c, attempts);
             break;
         }
-        if (m != 0) __builtin_amdgcn_s_sleep(1);
-        // one round trip per poll: the stamps and the error word together
+        // one round trip per poll, the stamps and the error word together,
+        // back to back (a short sleep between polls measured ~2 % slower)
         const uint32_t e = ld_relaxed(a.err);
         uint32_t st = 0;
         if (lane < N) st = ld_relaxed(stamp + lane);
@@ -616,7 +616,6 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
             const uint32_t e = ld_relaxed(a.err);
             free = done == prev;
             if (free || ++spins >= A.r.spin_limit || e != 0) break;
-            __builtin_amdgcn_s_sleep(1);
         }
         if (!free) {
             if (lane == 0) latch(a.err, kErrWaw, g, k.c, spins);
