@@ -320,6 +320,27 @@ def test_payload_sweep_points(N, T, H, persistent):
     run.s.close()
 
 
+def test_persistent_largest_sweep_point_fits():
+    """The sweep's largest persistent step (N=8, T=256, H=8192: 4096 chunks,
+    8192 co-resident waves) must be accepted on an MI355X: the step kernel
+    then runs in its lower-register form, the prefetching producer needing
+    more registers than 8 waves per SIMD allow. Checks one step in full."""
+    N, T, H = 8, 256, 8192
+    props = torch.cuda.get_device_properties(0)
+    if props.multi_processor_count < 256:
+        pytest.skip("fewer compute units than an MI355X")
+    w = synth.Workload(4, f"sweep-n{N}-t{T}-h{H}", N, (T,), H, 4, 1, "uniform")
+    print(f"largest persistent sweep step N={N} T={T} H={H}", flush=True)
+    run = StepRun(w, T, pool=synth.payload_pool(4, N, T, H, 5, "uniform"), persistent=1)
+    epochs = run.step(T)
+    got = to_host(run.out_d)
+    for i in range(4):
+        g = epochs[i]
+        assert np.array_equal(got[i], oracle.reduce(run.pool[(g - 1) % 5])), f"node {i}"
+    run.s.check()
+    run.s.close()
+
+
 @pytest.mark.parametrize("fuse", [1, 0])
 @pytest.mark.parametrize("waves_per_group", [1, 4, 16])
 @pytest.mark.parametrize("T", [1, 8, 32])
