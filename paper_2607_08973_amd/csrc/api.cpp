@@ -164,12 +164,17 @@ int launch_red(sifar_t h, const ReduceArgs &ra, const ProduceArgs *next, hipStre
 
 // Waves per workgroup of a persistent step. Grouping lets one publication
 // (and, for a cross-XCD pair, one release fence) cover 4 chunks and shares a
-// CU among 4 waves. Measured on MI355X with same-XCD pairs: it lengthens the
-// step up to 256 chunks (64 chunks: 0.92 -> 1.41 us per all-reduce) and
-// shortens it from 512 on (N = 8, 1024 chunks: 4.72 -> 3.68 us).
+// CU among 4 waves. Measured on MI355X with same-XCD pairs and the producer
+// loading each epoch's sources ahead (payload sweep, us per all-reduce,
+// one-wave vs grouped): plain steps at 512 chunks 1.81 vs 1.98 (N = 8), at
+// 1024 chunks 1.84 vs 1.98 (N = 2) but 4.32 vs 3.66 (N = 8), at 2048 chunks
+// 4.50 vs 3.84 (N = 2) and 10.5 vs 9.3 (N = 8); with the epilogue (MoE,
+// 512 chunks) 3.06 vs 2.80. So plain steps group from 1024 chunks at
+// N >= 8 and from 2048 below; epilogue steps from 512.
 int chain_waves(const sifar_ctx *h, int32_t tokens) {
     const int64_t chunks = static_cast<int64_t>(tokens) * h->segs;
-    return h->chain_grouping && h->segs % kChainGroupWaves == 0 && chunks >= 512
+    const int64_t from = h->cfg.epilogue ? 512 : (h->cfg.nranks >= 8 ? 1024 : 2048);
+    return h->chain_grouping && h->segs % kChainGroupWaves == 0 && chunks >= from
                ? kChainGroupWaves
                : 1;
 }
