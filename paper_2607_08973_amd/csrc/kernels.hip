@@ -836,9 +836,13 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
 // base+1 .. base+L in order, plane 1 produces it. The last wave to arrive on
 // the counter advances the epoch base for the next step: every wave read the
 // base before it arrived, so no wave can see the advanced value.
+// The plain grouped form is held to 64 VGPRs (8 waves per SIMD; 3 registers
+// spill, outside the epoch loop) so that the payload sweep's 4096-chunk step
+// (2048 four-wave groups) fits the GPU grouped: 22.4 -> 21.0 us per
+// all-reduce against the one-wave form it needed at 68 VGPRs.
 template <int N, int MODE, bool EPI, bool GROUPED, bool PREFETCH>
-__global__ __launch_bounds__(GROUPED ? kChainGroupWaves * kLanes : kLanes) void chain_kernel(
-    ChainArgs A) {
+__global__ __launch_bounds__(GROUPED ? kChainGroupWaves * kLanes : kLanes,
+                             GROUPED && !EPI ? 8 : 1) void chain_kernel(ChainArgs A) {
     const int lane = threadIdx.x & (kLanes - 1);
     const int wave = GROUPED ? static_cast<int>(threadIdx.x) / kLanes : 0;
     const int G = GROUPED ? static_cast<int>(blockDim.x) / kLanes : 1;
