@@ -183,6 +183,9 @@ def parse():
                     help="reduce-cold: waves per workgroup of the reduction kernel")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline (0 disables it)")
+    ap.add_argument("--wide-points", type=int, default=1,
+                    help="also time the chain at 16 and 64 tokens (1) or not (0: profiling "
+                         "runs, whose averages cover the headline launches only)")
     args = ap.parse_args()
     steps_persistent = args.persistent and args.workload not in ("ablation", "reduce-cold",
                                                                  "litmus")
@@ -651,7 +654,7 @@ def main():
     # would take 809 MB, and the peers' sources would come from HBM instead of
     # the Infinity Cache that holds the 8-token pool (101 MB).
     wide = {}
-    for T in (16, 64):
+    for T in ((16, 64) if args.wide_points else ()):
         pt = chain_point(w, T, args, T_max=T, pool_entries=5, check_nodes=(0, L // 2, -1))
         wide[str(T)] = round(pt["us_per_reduce"], 4) if "us_per_reduce" in pt else pt["skipped"]
 
