@@ -627,6 +627,8 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
             publish_slot(local);
         } else if (local) {
             store_slots<N>(a, k, p, cur);
+            // the loads stay after the stores (the wait below counts on it)
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);
             load_sources<N>(a, k, g + 1u, nxt);
             // Loads and stores complete in issue order on gfx9-family GPUs:
             // with at most N operations outstanding the slot stores have
