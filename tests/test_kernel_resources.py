@@ -1,0 +1,81 @@
+"""Register budgets of the persistent step kernels, checked at compile time.
+
+A persistent step needs every one of its waves resident at once. The payload
+sweep's largest step (N = 8, T = 256, H = 8192: 4096 chunks) fills an MI355X
+exactly: 8192 one-wave workgroups, or 2048 four-wave groups, i.e. 8 waves per
+SIMD, which gfx950 grants only to kernels of at most 64 VGPRs. Compiling the
+device code here (hipcc cross-compiles without a GPU) catches a change that
+pushes those kernels past the budget before a GPU run skips or refuses the
+step. No GPU is used.
+"""
+from __future__ import annotations
+
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+from paper_2607_08973_amd import build as B
+
+WAVES_PER_SIMD_AT_64_VGPRS = 64
+
+
+def _hipcc():
+    for cand in (shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
+        if cand and os.path.exists(cand):
+            return cand
+    return None
+
+
+@pytest.fixture(scope="module")
+def kernel_resources(tmp_path_factory):
+    """{mangled kernel name: {"vgpr": n, "spill": n}} from the device assembly."""
+    hipcc = _hipcc()
+    if hipcc is None:
+        pytest.skip("hipcc not available")
+    out = tmp_path_factory.mktemp("isa") / "kernels.s"
+    flags = [f for f in B.FLAGS if f not in ("-fPIC", "-shared")]
+    cmd = [hipcc, *flags, "--cuda-device-only", "-S", "-I", B.INCLUDE, "-I", B.CSRC,
+           os.path.join(B.CSRC, "kernels.hip"), "-o", str(out)]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    assert res.returncode == 0, res.stderr[-2000:]
+    text = out.read_text()
+    found = {}
+    # kernel metadata entries: ".name: <sym>" ... ".vgpr_count: n", ".vgpr_spill_count: n"
+    for m in re.finditer(r"\.name:\s+(\S+)\n(.*?)(?=\n\s+- \.|\n\s+-\s|\Z)", text, re.S):
+        body = m.group(2)
+        v = re.search(r"\.vgpr_count:\s+(\d+)", body)
+        if v:
+            s = re.search(r"\.vgpr_spill_count:\s+(\d+)", body)
+            found[m.group(1)] = {"vgpr": int(v.group(1)), "spill": int(s.group(1)) if s else 0}
+    assert found, "no kernel metadata in the device assembly"
+    return found
+
+
+def _chain(n, epi, grouped, prefetch):
+    b = lambda x: "1" if x else "0"
+    return (f"_ZN5sifar12_GLOBAL__N_112chain_kernelILi{n}ELi1ELb{b(epi)}ELb{b(grouped)}"
+            f"ELb{b(prefetch)}EEEvNS_9ChainArgsE")
+
+
+def test_largest_steps_fit_eight_waves_per_simd(kernel_resources):
+    """The non-prefetching one-wave kernel and the grouped kernel of a plain
+    N = 8 step stay within 64 VGPRs (the forms init falls back to, or groups
+    with, when a step needs every wave slot of the GPU)."""
+    for name in (_chain(8, False, False, False), _chain(8, False, True, False)):
+        assert name in kernel_resources, name
+        assert kernel_resources[name]["vgpr"] <= WAVES_PER_SIMD_AT_64_VGPRS, (
+            name, kernel_resources[name])
+
+
+def test_prefetching_kernel_keeps_its_occupancy(kernel_resources):
+    """The prefetching one-wave kernel (the llama8b decode step's) holds two
+    epochs' sources. At most 128 VGPRs keeps 4 waves per SIMD, enough for
+    one-wave steps of up to 2048 chunks (larger handles fall back to the
+    non-prefetching form), and it does not spill."""
+    name = _chain(8, False, False, True)
+    assert name in kernel_resources, name
+    r = kernel_resources[name]
+    assert r["vgpr"] <= 128 and r["spill"] == 0, (name, r)
