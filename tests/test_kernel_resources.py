@@ -19,7 +19,7 @@ import pytest
 
 from paper_2607_08973_amd import build as B
 
-WAVES_PER_SIMD_AT_64_VGPRS = 64
+VGPRS_FOR_8_WAVES_PER_SIMD = 64
 
 
 def _hipcc():
@@ -66,7 +66,7 @@ def test_largest_steps_fit_eight_waves_per_simd(kernel_resources):
     with, when a step needs every wave slot of the GPU)."""
     for name in (_chain(8, False, False, False), _chain(8, False, True, False)):
         assert name in kernel_resources, name
-        assert kernel_resources[name]["vgpr"] <= WAVES_PER_SIMD_AT_64_VGPRS, (
+        assert kernel_resources[name]["vgpr"] <= VGPRS_FOR_8_WAVES_PER_SIMD, (
             name, kernel_resources[name])
 
 
