@@ -341,6 +341,29 @@ def test_persistent_largest_sweep_point_fits():
     run.s.close()
 
 
+def test_persistent_small_steps_on_a_full_size_handle():
+    """A handle sized for the sweep's largest step (N=8, T_max=256, H=8192)
+    cannot hold the prefetching one-wave kernel's waves at T_max, so its
+    one-wave steps run the non-prefetching form. Steps of 1 and 8 tokens
+    (16 and 128 chunks, one wave per chunk) on it, every output checked."""
+    N, T_max, H = 8, 256, 8192
+    props = torch.cuda.get_device_properties(0)
+    if props.multi_processor_count < 256:
+        pytest.skip("fewer compute units than an MI355X")
+    w = synth.Workload(4, f"sweep-n{N}-t{T_max}-h{H}", N, (T_max,), H, 4, 1, "uniform")
+    print(f"small persistent steps on a handle for N={N} T_max={T_max} H={H}", flush=True)
+    run = StepRun(w, T_max, pool=synth.payload_pool(4, N, T_max, H, 5, "uniform"), persistent=1)
+    for T in (1, 8):
+        epochs = run.step(T)
+        got = to_host(run.out_d)
+        for i in range(4):
+            g = epochs[i]
+            assert np.array_equal(got[i, :T], oracle.reduce(run.pool[(g - 1) % 5][:, :T])), \
+                f"T={T} node {i}"
+        run.s.check()
+    run.s.close()
+
+
 @pytest.mark.parametrize("fuse", [1, 0])
 @pytest.mark.parametrize("waves_per_group", [1, 4, 16])
 @pytest.mark.parametrize("T", [1, 8, 32])
