@@ -610,12 +610,16 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
         const size_t pc = static_cast<size_t>(p) * geo.w_max + k.c;
         uint32_t spins = 0;
         bool free = false;
-        while (true) {  // one round trip per poll: both words and the error word together
+        // one round trip per poll: both words and the error word together; a
+        // short sleep between polls (without it the kernel takes 109 VGPRs
+        // instead of 76 and the step ran ~0.6 % slower)
+        while (true) {
             const uint32_t done = ld_relaxed(a.consumed + pc);
             const uint32_t prev = ld_relaxed(a.produced + pc);
             const uint32_t e = ld_relaxed(a.err);
             free = done == prev;
             if (free || ++spins >= A.r.spin_limit || e != 0) break;
+            __builtin_amdgcn_s_sleep(1);
         }
         if (!free) {
             if (lane == 0) latch(a.err, kErrWaw, g, k.c, spins);

@@ -72,10 +72,11 @@ def test_largest_steps_fit_eight_waves_per_simd(kernel_resources):
 
 def test_prefetching_kernel_keeps_its_occupancy(kernel_resources):
     """The prefetching one-wave kernel (the llama8b decode step's) holds two
-    epochs' sources. At most 128 VGPRs keeps 4 waves per SIMD, enough for
-    one-wave steps of up to 2048 chunks (larger handles fall back to the
-    non-prefetching form), and it does not spill."""
+    epochs' sources. At most 80 VGPRs keeps 6 waves per SIMD, enough for
+    one-wave steps of up to 3072 chunks (larger handles fall back to the
+    non-prefetching form), and it does not spill. (A producer slot wait
+    without its short sleep once took it to 109.)"""
     name = _chain(8, False, False, True)
     assert name in kernel_resources, name
     r = kernel_resources[name]
-    assert r["vgpr"] <= 128 and r["spill"] == 0, (name, r)
+    assert r["vgpr"] <= 80 and r["spill"] == 0, (name, r)
