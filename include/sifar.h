@@ -373,6 +373,43 @@ typedef struct {
 int sifar_litmus(int32_t protocol, int32_t placement, int32_t pairs, int32_t trials,
                  void *stream, sifar_litmus_result *result);
 
+/* ---- Allocation-free all-reduce ---------------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc. One
+ * all-reduce of `tokens` x `hidden` bf16 over `nranks` emulated ranks, the work
+ * of sifar_produce followed by sifar_reduce on a SIFAR_VALIDATE_SPEC handle,
+ * without a handle: the emulated peers copy rank r's partial
+ * (src + r * src_rank_stride elements, laid out [tokens][hidden]) into a slot
+ * and stamp it with the call's epoch, then the speculative reduction
+ * validates the stamps and writes the fixed-order fp32 sum, rounded to bf16,
+ * to out[tokens][hidden]. Two kernel launches on `stream`; nothing is
+ * allocated or freed (no hipMalloc, hipFree or other allocating call), and
+ * nothing synchronises.
+ *
+ * Scratch: the library's state for this call (slots, stamps, consumed and
+ * produced words, decision log, epoch and error words) lives in one static
+ * device array of SIFAR_NOALLOC_SCRATCH_BYTES per GPU, held from the first
+ * call on that GPU until the process ends. Every call on a GPU shares that
+ * GPU's array and leaves its contents behind; epochs grow from call to call
+ * (host-side count per device), so a stamp of an earlier call is always
+ * stale. Calls that overlap on one GPU (other streams, other host threads
+ * without ordering) race on the array and may return wrong sums; calls
+ * ordered on one stream never do, and then the producer's launch completes
+ * before the reduction's, so no validation fails and no device error arises.
+ *
+ * Limits: 1 <= nranks <= 8; hidden a multiple of 8 in 8..65536;
+ * 1 <= tokens <= SIFAR_NOALLOC_MAX_TOKENS; tokens * hidden <=
+ * SIFAR_NOALLOC_MAX_ELEMS (512 KiB of bf16 per rank: 64 tokens x 4096);
+ * src_rank_stride >= tokens * hidden and a multiple of 8; src and out 16-byte
+ * aligned device pointers on the current device. Anything else returns
+ * SIFAR_EINVAL before any work is enqueued; SIFAR_EHIP if a launch or the
+ * symbol lookup fails. */
+#define SIFAR_NOALLOC_MAX_TOKENS 64
+#define SIFAR_NOALLOC_MAX_ELEMS 262144
+#define SIFAR_NOALLOC_SCRATCH_BYTES 8437248 /* 8 MiB of slots + 47.5 KiB of words */
+int sifar_allreduce_noalloc(const void *src, int64_t src_rank_stride, int32_t nranks,
+                            int32_t tokens, int32_t hidden, void *out, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -59,6 +59,11 @@ SIFAR_LITMUS_READ_FIRST = 1
 SIFAR_LITMUS_CROSS_XCD = 0
 SIFAR_LITMUS_SAME_XCD = 1
 
+# the allocation-free entry point's limits and its static array
+SIFAR_NOALLOC_MAX_TOKENS = 64
+SIFAR_NOALLOC_MAX_ELEMS = 262144
+SIFAR_NOALLOC_SCRATCH_BYTES = 8437248
+
 CHUNK = 512  # elements per chunk (one 64-lane wave, 16 bytes per lane)
 
 # every symbol include/sifar.h declares
@@ -67,7 +72,7 @@ EXPORTS = (
     "sifar_produce", "sifar_reduce", "sifar_reduce_rmsnorm", "sifar_bind_step",
     "sifar_step", "sifar_set_injection", "sifar_log_geometry", "sifar_read_log",
     "sifar_epochs", "sifar_status", "sifar_error_info", "sifar_strerror", "sifar_floor",
-    "sifar_litmus",
+    "sifar_litmus", "sifar_allreduce_noalloc",
 )
 
 
@@ -166,6 +171,7 @@ def load(path: str = LIB_PATH):
                                        ctypes.POINTER(U32)]),
         "sifar_litmus": (ctypes.c_int, [I32, I32, I32, I32, P,
                                         ctypes.POINTER(sifar_litmus_result)]),
+        "sifar_allreduce_noalloc": (ctypes.c_int, [P, I64, I32, I32, I32, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -308,6 +314,13 @@ def sifar_litmus(protocol: int, placement: int, pairs: int, trials: int, stream=
         err.result = out
         raise err
     return out
+
+
+def sifar_allreduce_noalloc(src, src_rank_stride: int, nranks: int, tokens: int, hidden: int,
+                            out, stream=None) -> None:
+    """One all-reduce on the library's static scratch (no allocation)."""
+    _check("sifar_allreduce_noalloc", load().sifar_allreduce_noalloc(
+        _ptr(src), src_rank_stride, nranks, tokens, hidden, _ptr(out), _stream(stream)))
 
 
 def sifar_status(h: int) -> int:

@@ -15,7 +15,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libsifar.so")
 SOURCES = [os.path.join(CSRC, "kernels.hip"), os.path.join(CSRC, "floors.hip"),
-           os.path.join(CSRC, "litmus.hip"), os.path.join(CSRC, "api.cpp")]
+           os.path.join(CSRC, "litmus.hip"), os.path.join(CSRC, "noalloc.hip"),
+           os.path.join(CSRC, "api.cpp")]
 ARCH = "gfx950"
 
 FLAGS = [

@@ -172,3 +172,21 @@ def test_struct_offsets_match_a_c_compiler(tmp_path):
         cls = structs[name]
         want = ctypes.sizeof(cls) if what == "size" else getattr(cls, what).offset
         assert int(value) == want, line
+
+
+@pytest.mark.parametrize("nranks,tokens,hidden,stride,misalign", [
+    (0, 1, 4096, 4096, 0), (9, 1, 4096, 4096, 0),          # ranks
+    (2, 0, 4096, 4096, 0), (2, 65, 4096, 65 * 4096, 0),    # tokens
+    (2, 1, 4100, 4100, 0), (2, 1, 0, 8, 0),                # hidden
+    (2, 64, 8192, 64 * 8192, 0),                           # beyond the static array
+    (2, 2, 4096, 4096, 0), (2, 1, 4096, 4100, 0),          # rank stride
+    (2, 1, 4096, 4096, 8),                                 # 8-byte aligned pointers
+])
+def test_noalloc_rejects_out_of_range_calls_on_host(nranks, tokens, hidden, stride, misalign):
+    """The allocation-free entry point refuses, before any device call, every
+    size its static array cannot hold and every malformed argument."""
+    L = S.load()
+    buf = ctypes.create_string_buffer(64)
+    p = (ctypes.addressof(buf) + 15) // 16 * 16 + misalign
+    assert L.sifar_allreduce_noalloc(p, stride, nranks, tokens, hidden, p, None) == S.SIFAR_EINVAL
+    assert L.sifar_allreduce_noalloc(None, 4096, 2, 1, 4096, p, None) == S.SIFAR_EINVAL
