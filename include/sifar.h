@@ -98,9 +98,14 @@ typedef struct sifar_ctx *sifar_t;
 
 /* ---- stale-stamp injection ---------------------------------------------------
  * DETERMINISTIC: for epoch g, table entry (g - 1) % entries holds two rank masks:
- *   bits 0-7  late ranks: the producer writes their payload but not their stamp;
- *             the stamp lands right after the reduction's first failed
- *             validation of each chunk (the rank "catches up").
+ *   bits 0-7  late ranks. Per-epoch launches: the producer writes their
+ *             payload into a library-owned stage, not their slot (which keeps
+ *             the rank's previous epoch), and writes no stamp; right after the
+ *             reduction's first failed validation of each chunk the rank
+ *             "catches up": its payload moves into the slot and, after a
+ *             release, its stamp is written, so the retry must reload the
+ *             payload. Persistent steps: the payload is written on time and
+ *             the stamp lands late_delay sleeps later.
  *   bits 8-15 withheld ranks: the stamp is never written; the chunk exhausts
  *             max_attempts and SIFAR_DEV_RETRY_BUDGET is latched.
  * The resulting per-chunk decisions are exactly predictable (see the log). */
@@ -264,6 +269,17 @@ int sifar_log_geometry(sifar_t h, int32_t *log_epochs, int32_t *chunks_per_token
  * log_epochs * w_max. */
 int sifar_read_log(sifar_t h, uint32_t *host_dst, size_t words);
 
+/* Copy the raw-stamp log to host memory (synchronises the device). Beside
+ * each decision word the library keeps the N stamps the chunk's first and
+ * last validation saw, so that every logged stale-rank mask can be
+ * recomputed from them (Sec. 4.2: validation compares each rank's flag with
+ * the epoch; Sec. 6.3 measures the mis-speculation rate). Same ring as the
+ * decision log: epoch g, chunk c, validation v (0 first, 1 last), rank r ->
+ * word (((g - 1) % log_epochs) * w_max + c) * 2N + v * N + r. In NONE mode no
+ * stamp is read and the words are 0. `words` must be at most
+ * log_epochs * w_max * 2N. */
+int sifar_read_stamp_log(sifar_t h, uint32_t *host_dst, size_t words);
+
 /* Next epoch to produce and next epoch to reduce (host-side accounting). */
 int sifar_epochs(sifar_t h, uint32_t *next_produce, uint32_t *next_reduce);
 
@@ -340,7 +356,14 @@ int sifar_floor(int32_t kind, int32_t iterations, void *stream, double *ns_per_o
  *            acquire, then the payload -- the persistent step's reader;
  *            SIFAR_LITMUS_READ_FIRST: payload and stamps loaded together and
  *            accepted when every stamp is fresh -- the paper's speculative
- *            reader (a stale stamp leads to an acquire and a reload of both)
+ *            reader (a stale stamp leads to an acquire and a reload of both);
+ *            SIFAR_LITMUS_ORDERED_PREFETCH: the ORDERED reader against a
+ *            producer that publishes as the persistent step's prefetching
+ *            producer does: buffer stores of the slot, buffer loads of the
+ *            next epoch's sources, a wait until only those loads are
+ *            outstanding (on one XCD; a release fence across XCDs), then the
+ *            flags. The other two protocols' producer stores the slot and
+ *            waits for everything it has outstanding.
  *  placement SIFAR_LITMUS_CROSS_XCD: producer and consumer on different XCDs;
  *            SIFAR_LITMUS_SAME_XCD: on one XCD (workgroups are dealt to the 8
  *            XCDs round robin; the waves read where they actually ran)
@@ -352,12 +375,13 @@ int sifar_floor(int32_t kind, int32_t iterations, void *stream, double *ns_per_o
  * gave up, how many pairs landed as asked, the consumers' mean nanoseconds per
  * trial, and for the first violation {epoch, word found, word expected,
  * (producer XCD << 8) | consumer XCD}. Synchronises `stream`; allocates and
- * frees its own device memory (16 KiB per pair plus control words). Returns
+ * frees its own device memory (24 KiB per pair plus control words). Returns
  * SIFAR_EINVAL for a bad argument, SIFAR_ENOMEM, SIFAR_EHIP, or SIFAR_EDEVICE
  * when a wait gave up (the result is still filled in). Violations are data,
  * not an error. */
 #define SIFAR_LITMUS_ORDERED 0
 #define SIFAR_LITMUS_READ_FIRST 1
+#define SIFAR_LITMUS_ORDERED_PREFETCH 2
 #define SIFAR_LITMUS_CROSS_XCD 0
 #define SIFAR_LITMUS_SAME_XCD 1
 typedef struct {

@@ -56,6 +56,7 @@ SIFAR_FLOOR_PINGPONG_SAME_XCD = 9
 
 SIFAR_LITMUS_ORDERED = 0
 SIFAR_LITMUS_READ_FIRST = 1
+SIFAR_LITMUS_ORDERED_PREFETCH = 2
 SIFAR_LITMUS_CROSS_XCD = 0
 SIFAR_LITMUS_SAME_XCD = 1
 
@@ -71,6 +72,7 @@ EXPORTS = (
     "sifar_config_default", "sifar_version", "sifar_init", "sifar_destroy",
     "sifar_produce", "sifar_reduce", "sifar_reduce_rmsnorm", "sifar_bind_step",
     "sifar_step", "sifar_set_injection", "sifar_log_geometry", "sifar_read_log",
+    "sifar_read_stamp_log",
     "sifar_epochs", "sifar_status", "sifar_error_info", "sifar_strerror", "sifar_floor",
     "sifar_litmus", "sifar_allreduce_noalloc",
 )
@@ -163,6 +165,7 @@ def load(path: str = LIB_PATH):
         "sifar_log_geometry": (ctypes.c_int, [P, ctypes.POINTER(I32), ctypes.POINTER(I32),
                                               ctypes.POINTER(I32)]),
         "sifar_read_log": (ctypes.c_int, [P, P, SZ]),
+        "sifar_read_stamp_log": (ctypes.c_int, [P, P, SZ]),
         "sifar_epochs": (ctypes.c_int, [P, ctypes.POINTER(U32), ctypes.POINTER(U32)]),
         "sifar_status": (ctypes.c_int, [P]),
         "sifar_error_info": (ctypes.c_int, [P, ctypes.POINTER(U32)]),
@@ -281,6 +284,16 @@ def sifar_read_log(h: int):
     return out
 
 
+def sifar_read_stamp_log(h: int, nranks: int):
+    """Raw stamps of each chunk's first and last validation, flat
+    ([log_epochs][w_max][2][N] in the header's order)."""
+    import numpy as np
+    epochs, _, w_max = sifar_log_geometry(h)
+    out = np.zeros(epochs * w_max * 2 * nranks, dtype=np.uint32)
+    _check("sifar_read_stamp_log", load().sifar_read_stamp_log(h, out.ctypes.data, out.size))
+    return out
+
+
 def sifar_epochs(h: int):
     a, b = ctypes.c_uint32(), ctypes.c_uint32()
     _check("sifar_epochs", load().sifar_epochs(h, ctypes.byref(a), ctypes.byref(b)))
@@ -386,6 +399,9 @@ class Sifar:
 
     def read_log(self):
         return sifar_read_log(self.h)
+
+    def read_stamp_log(self):
+        return sifar_read_stamp_log(self.h, self.cfg.nranks)
 
     def log_geometry(self):
         return sifar_log_geometry(self.h)

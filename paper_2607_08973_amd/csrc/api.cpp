@@ -27,6 +27,8 @@ struct sifar_ctx {
     uint32_t *consumed = nullptr;  // [2][w_max]
     uint32_t *produced = nullptr;  // [2][w_max]
     uint32_t *log = nullptr;       // [log_epochs][w_max]
+    uint32_t *stamp_log = nullptr; // [log_epochs][w_max][2][N]
+    uint16_t *stage = nullptr;     // [N][2][slot_elems]: late ranks' payload (deterministic injection)
     uint64_t *exch = nullptr;      // [kExchPlanes][max_tokens][exch_q]
     uint64_t *place = nullptr;     // [2][w_max] XCD tags of each chunk's consumer / producer
     int exch_q = 1;                // exchange words per token and parity
@@ -126,6 +128,7 @@ ProduceArgs produce_args(const sifar_t h, int32_t tokens, EpochRef ep, const uin
     a.entries = entries;
     a.inject = h->inject;
     a.inject_entries = h->inject_entries;
+    a.stage = h->inject ? h->stage : nullptr;
     a.err = h->state->err;
     return a;
 }
@@ -138,12 +141,14 @@ ReduceArgs reduce_args(const sifar_t h, int32_t tokens, EpochRef ep) {
     a.stamps = h->stamps;
     a.consumed = h->consumed;
     a.log = h->log;
+    a.stamp_log = h->stamp_log;
     a.log_epochs = h->cfg.log_epochs;
     a.max_attempts = h->cfg.max_attempts;
     a.forced_retries = h->cfg.forced_retries;
     a.spin_limit = h->cfg.spin_limit;
     a.inject = h->inject;
     a.inject_entries = h->inject_entries;
+    a.stage = h->inject ? h->stage : nullptr;
     a.exch = h->exch;
     a.groups_per_token = h->groups_per_token;
     a.exch_parity_stride = h->cfg.max_tokens * h->exch_q;
@@ -188,6 +193,10 @@ int chain_args(const sifar_t h, int32_t tokens, ChainArgs *ca) {
     ca->p = produce_args(h, tokens, ep, static_cast<const uint16_t *>(h->buf.src_pool),
                          h->buf.pool_entry_stride, h->buf.pool_rank_stride, h->buf.pool_entries);
     ca->r = reduce_args(h, tokens, ep);
+    // a persistent step's late ranks write their payload on time and delay
+    // only their stamps (late_delay): nothing is staged
+    ca->p.stage = nullptr;
+    ca->r.stage = nullptr;
     if (h->cfg.epilogue) {
         ca->r.residual = static_cast<uint16_t *>(h->buf.residual);
         ca->r.weight = static_cast<const uint16_t *>(h->buf.weight);
@@ -361,6 +370,9 @@ int sifar_init(const sifar_config *cfg, sifar_t *out) {
     if (!rc) rc = dev_alloc(&h->consumed, static_cast<size_t>(2) * h->w_max);
     if (!rc) rc = dev_alloc(&h->produced, static_cast<size_t>(2) * h->w_max);
     if (!rc) rc = dev_alloc(&h->log, static_cast<size_t>(c.log_epochs) * h->w_max);
+    if (!rc)
+        rc = dev_alloc(&h->stamp_log,
+                       static_cast<size_t>(c.log_epochs) * h->w_max * 2 * c.nranks);
     if (!rc) rc = dev_alloc(&h->exch, static_cast<size_t>(kExchPlanes) * c.max_tokens * h->exch_q);
     if (!rc) rc = dev_alloc(&h->place, static_cast<size_t>(2) * h->w_max);
     if (!rc) rc = dev_alloc(&h->state, 1);
@@ -376,6 +388,9 @@ int sifar_init(const sifar_config *cfg, sifar_t *out) {
         if (e == hipSuccess) e = launch_fill_u32(h->produced, 0, static_cast<uint64_t>(2) * h->w_max, s);
         if (e == hipSuccess)
             e = launch_fill_u32(h->log, 0, static_cast<uint64_t>(c.log_epochs) * h->w_max, s);
+        if (e == hipSuccess)
+            e = launch_fill_u32(h->stamp_log, 0,
+                                static_cast<uint64_t>(c.log_epochs) * h->w_max * 2 * c.nranks, s);
         if (e == hipSuccess)
             e = launch_fill_u32(reinterpret_cast<uint32_t *>(h->exch), 0,
                                 static_cast<uint64_t>(kExchPlanes) * c.max_tokens * h->exch_q * 2,
@@ -407,6 +422,8 @@ void sifar_destroy(sifar_t h) {
     (void)hipFree(h->consumed);
     (void)hipFree(h->produced);
     (void)hipFree(h->log);
+    (void)hipFree(h->stamp_log);
+    (void)hipFree(h->stage);
     (void)hipFree(h->exch);
     (void)hipFree(h->place);
     (void)hipFree(h->state);
@@ -568,6 +585,11 @@ int sifar_set_injection(sifar_t h, const uint16_t *table, int32_t entries, int32
     }
     if (!table || entries < 1) return SIFAR_EINVAL;
     if (hipDeviceSynchronize() != hipSuccess) return SIFAR_EHIP;
+    // where late ranks' payloads wait until they catch up (per-epoch launches)
+    if (!h->stage) {
+        rc = dev_alloc(&h->stage, static_cast<size_t>(h->cfg.nranks) * 2 * h->slot_elems);
+        if (rc) return rc;
+    }
     uint16_t *d = nullptr;
     rc = dev_alloc(&d, static_cast<size_t>(entries));
     if (rc) return rc;
@@ -595,6 +617,17 @@ int sifar_read_log(sifar_t h, uint32_t *host_dst, size_t words) {
     if (words > static_cast<size_t>(h->cfg.log_epochs) * h->w_max) return SIFAR_EINVAL;
     if (hipDeviceSynchronize() != hipSuccess) return SIFAR_EHIP;
     if (hipMemcpy(host_dst, h->log, words * sizeof(uint32_t), hipMemcpyDeviceToHost) != hipSuccess)
+        return SIFAR_EHIP;
+    return SIFAR_OK;
+}
+
+int sifar_read_stamp_log(sifar_t h, uint32_t *host_dst, size_t words) {
+    if (!h || !host_dst) return SIFAR_EINVAL;
+    if (words > static_cast<size_t>(h->cfg.log_epochs) * h->w_max * 2 * h->cfg.nranks)
+        return SIFAR_EINVAL;
+    if (hipDeviceSynchronize() != hipSuccess) return SIFAR_EHIP;
+    if (hipMemcpy(host_dst, h->stamp_log, words * sizeof(uint32_t), hipMemcpyDeviceToHost) !=
+        hipSuccess)
         return SIFAR_EHIP;
     return SIFAR_OK;
 }

@@ -65,8 +65,6 @@ __device__ void latch(uint32_t *err, uint32_t kind, uint32_t g, uint32_t c, uint
     }
 }
 
-__device__ __forceinline__ bool latched(const uint32_t *err) { return ld_relaxed(err) != 0; }
-
 constexpr uint32_t kErrRetryBudget = 1, kErrWaw = 2, kErrExchange = 3;
 
 // Where the calling lane works: token t, chunk s of the row, chunk index c.
@@ -98,6 +96,13 @@ __device__ __forceinline__ Chunk chunk_at(const Geometry &geo, int t, int s, int
 __device__ __forceinline__ uint32_t log_word(uint32_t attempts, uint32_t first, uint32_t last) {
     return (attempts > 0xFFFFu ? 0xFFFFu : attempts) | ((first & 0xFFu) << 16) |
            ((last & 0xFFu) << 24);
+}
+
+// Ranks the injection table makes late (not withheld) at epoch g.
+__device__ __forceinline__ uint32_t late_ranks(const uint16_t *inject, int32_t entries, uint32_t g) {
+    if (!inject) return 0;
+    const uint32_t inj = inject[(g - 1u) % static_cast<uint32_t>(entries)];
+    return inj & ~(inj >> 8) & 0xFFu;
 }
 
 // ---------------------------------------------------------------------------
@@ -141,20 +146,25 @@ __device__ __forceinline__ void store_slots(const ProduceArgs &a, const Chunk &k
 
 // Copy every rank's part of chunk k of epoch g into the slots of parity p
 // (the producers that load and store in one go; plain global addressing
-// measured faster for them than the buffer form above).
+// measured faster for them than the buffer form above). Ranks in `staged`
+// (wave-uniform) write into the stage instead: they are late, and their slot
+// keeps its previous epoch until they catch up.
 template <int N>
 __device__ __forceinline__ void copy_chunk(const ProduceArgs &a, const Chunk &k, uint32_t g,
-                                           uint32_t p) {
+                                           uint32_t p, uint32_t staged = 0) {
     const Geometry &geo = a.geo;
     const uint32_t e = (g - 1u) % static_cast<uint32_t>(a.entries);
     const uint16_t *src = a.src + e * a.entry_stride + static_cast<int64_t>(k.row);
-    uint16_t *dst = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + k.row;
+    const uint64_t at = static_cast<uint64_t>(p) * geo.slot_elems + k.row;
     V16 v[N];
 #pragma unroll
     for (int r = 0; r < N; ++r) v[r] = ld16(src + r * a.rank_stride);
     if (k.lane_ok) {
 #pragma unroll
-        for (int r = 0; r < N; ++r) st16(dst + r * 2 * geo.slot_elems, v[r]);
+        for (int r = 0; r < N; ++r) {
+            uint16_t *dst = ((staged >> r) & 1u) ? a.stage : a.slots;
+            st16(dst + at + r * 2 * geo.slot_elems, v[r]);
+        }
     }
 }
 
@@ -165,7 +175,9 @@ __device__ __forceinline__ uint32_t held_back(const uint16_t *inject, int32_t en
     return (inj | (inj >> 8)) & 0xFFu;
 }
 
-// Producer of one epoch in its own launch (eager calls, step graphs). The
+// Producer of one epoch in its own launch (eager calls, step graphs). With
+// deterministic injection a late rank's payload goes to the stage and its
+// stamp is not written: the rank has not caught up yet. The
 // stamp stores are ordered after the payload stores of the wave
 // (workgroup-scope release); device-wide visibility comes from the end of the
 // launch, because the reduction of an epoch always runs in a later launch than
@@ -190,9 +202,9 @@ __device__ __forceinline__ void produce_chunk(const ProduceArgs &a) {
     // Dual-buffer rule: the slot's previous epoch must have been consumed.
     const uint32_t prev = ld_relaxed(a.produced + pc);
     const uint32_t done = ld_relaxed(a.consumed + pc);
-    copy_chunk<N>(a, k, g, p);
-    if (lane == 0 && prev != done) latch(a.err, kErrWaw, g, k.c, prev);
     const uint32_t held = held_back(a.inject, a.inject_entries, g);
+    copy_chunk<N>(a, k, g, p, a.stage ? late_ranks(a.inject, a.inject_entries, g) : 0u);
+    if (lane == 0 && prev != done) latch(a.err, kErrWaw, g, k.c, prev);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     uint32_t *stamp = a.stamps + pc * N;
     if (lane < N && !((held >> lane) & 1u)) st_relaxed(stamp + lane, g);
@@ -214,14 +226,18 @@ __device__ __forceinline__ void load_payload(V16 (&v)[N], const uint16_t *slot0,
 }
 
 // Gather of a per-epoch launch: load chunk k of epoch g, validate its N
-// stamps, retry while any is stale. The epoch's payload was written by an
-// earlier launch, so a stale stamp can only be an injected late one.
-// INJECT_HOOK: deterministic injection, the late ranks' stamps land right
-// after the first failed validation.
+// stamps, retry while any is stale. The epoch's on-time payload was written by
+// an earlier launch, so a stale stamp can only be an injected late one.
+// INJECT_HOOK: deterministic injection, the late ranks catch up right after
+// the first failed validation: their payload moves from the stage into the
+// slot (which still held their previous epoch when it was first loaded),
+// then, after a release, their stamps are written. The retry must therefore
+// reload the payload to get the right sum. `st_first` / `st_last`: this
+// lane's stamp (lanes < N) at the first and at the last validation.
 template <int N, int MODE, bool INJECT_HOOK>
 __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint32_t g, uint32_t p,
                                        int lane, V16 (&v)[N], uint32_t &attempts, uint32_t &first,
-                                       uint32_t &last) {
+                                       uint32_t &last, uint32_t &st_first, uint32_t &st_last) {
     const Geometry &geo = a.geo;
     const uint16_t *slot0 = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + k.row;
     const uint64_t rank_step = 2 * geo.slot_elems;  // slots are [rank][parity]
@@ -234,6 +250,7 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
         load_payload<N>(v, slot0, rank_step);
         if (MODE == kSpec && k.active && lane < N) st = ld_relaxed(stamp + lane);
     }
+    st_first = st;
 
     attempts = 1;
     first = last = 0;
@@ -247,9 +264,20 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
                 break;
             }
             if (INJECT_HOOK && attempts == 1 && a.inject && m != 0) {
-                const uint32_t inj = a.inject[(g - 1u) % static_cast<uint32_t>(a.inject_entries)];
-                if (lane < N && ((inj >> lane) & 1u) && !((inj >> (8 + lane)) & 1u))
-                    st_release(stamp + lane, g);
+                const uint32_t late = late_ranks(a.inject, a.inject_entries, g);
+                if (a.stage) {
+                    const uint64_t at = static_cast<uint64_t>(p) * geo.slot_elems + k.row;
+#pragma unroll
+                    for (int r = 0; r < N; ++r) {
+                        if ((late >> r) & 1u) {
+                            const V16 x = ld16(a.stage + at + r * rank_step);
+                            if (k.lane_ok) st16(a.slots + at + r * rank_step, x);
+                        }
+                    }
+                }
+                // the payload is published before the stamps, as a peer would
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+                if (lane < N && ((late >> lane) & 1u)) st_relaxed(stamp + lane, g);
             }
             // plain reloads need an acquire fence (an L2 invalidate) to see the
             // peers' data
@@ -266,19 +294,22 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
             fail = m != 0 || attempts <= a.forced_retries;
         }
     }
+    st_last = st;
     if (MODE == kOrdered) load_payload<N>(v, slot0, rank_step);
 }
 
 // Persistent-step gather of an active chunk: a producer may be writing right
 // now, so only ORDERED is sound. `m` is the stale-rank mask of the first stamp
-// poll (issued and evaluated by the caller); polls repeat (relaxed agent-scope
-// loads) until every stamp is fresh, then the payload is loaded
-// -- after an acquire fence when the producer is on another XCD, directly when
-// it shares this XCD (see publish_slot).
+// poll and `st` this lane's stamp from it (issued and evaluated by the
+// caller); polls repeat (relaxed agent-scope loads; lanes >= N read rank
+// N - 1's, which the ballot ignores) until every stamp is fresh, then the
+// payload is loaded -- after an acquire fence when the producer is on another
+// XCD, directly when it shares this XCD (see publish_slot). On return `st`
+// holds the stamp of the last poll.
 template <int N>
 __device__ __forceinline__ void gather_chain(const ReduceArgs &a, const Chunk &k, uint32_t g,
-                                             uint32_t p, int lane, uint32_t m, V16 (&v)[N],
-                                             uint32_t &attempts, uint32_t &first,
+                                             uint32_t p, int lane, uint32_t m, uint32_t &st,
+                                             V16 (&v)[N], uint32_t &attempts, uint32_t &first,
                                              uint32_t &last, bool local) {
     const Geometry &geo = a.geo;
     // the chunk's first element in rank 0's slot (wave-uniform) and this
@@ -287,7 +318,8 @@ __device__ __forceinline__ void gather_chain(const ReduceArgs &a, const Chunk &k
         a.slots + static_cast<uint64_t>(p) * geo.slot_elems + chunk_first(geo, k);
     const uint32_t off = lane_offset(geo, k);
     const uint64_t rank_step = 2 * geo.slot_elems;  // slots are [rank][parity]
-    const uint32_t *stamp = a.stamps + (static_cast<size_t>(p) * geo.w_max + k.c) * N;
+    const uint32_t *stamp = a.stamps + (static_cast<size_t>(p) * geo.w_max + k.c) * N +
+                            (lane < N ? lane : N - 1);
     attempts = 1;
     first = last = m;
     bool fail = m != 0 || a.forced_retries >= 1;
@@ -299,8 +331,7 @@ __device__ __forceinline__ void gather_chain(const ReduceArgs &a, const Chunk &k
         // one round trip per poll, the stamps and the error word together,
         // back to back (a short sleep between polls measured ~2 % slower)
         const uint32_t e = ld_relaxed(a.err);
-        uint32_t st = 0;
-        if (lane < N) st = ld_relaxed(stamp + lane);
+        st = ld_relaxed(stamp);
         ++attempts;
         m = static_cast<uint32_t>(__ballot(lane < N && st != g));
         last = m;
@@ -339,6 +370,18 @@ __device__ __forceinline__ void write_log(const ReduceArgs &a, const Chunk &k, u
                                           uint32_t word) {
     a.log[static_cast<size_t>((g - 1u) % static_cast<uint32_t>(a.log_epochs)) * a.geo.w_max + k.c] =
         word;
+}
+
+// Rank r's raw stamp at the chunk's first and last validation, beside the
+// decision word, so that every logged mask can be recomputed from the stamps.
+template <int N>
+__device__ __forceinline__ void write_stamp_log(const ReduceArgs &a, const Chunk &k, uint32_t g,
+                                                int r, uint32_t first, uint32_t last) {
+    uint32_t *row = a.stamp_log +
+                    (static_cast<size_t>((g - 1u) % static_cast<uint32_t>(a.log_epochs)) *
+                         a.geo.w_max + k.c) * (2 * N) + r;
+    row[0] = first;
+    row[N] = last;
 }
 
 // Residual-add + RMSNorm of one chunk after its all-reduce result o. The
@@ -449,13 +492,14 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
     }
     const uint32_t g = epoch_of(a.ep);
     V16 v[N];
-    uint32_t attempts, first, last;
-    gather<N, MODE, true>(a, k, g, p, lane, v, attempts, first, last);
+    uint32_t attempts, first, last, st_first, st_last;
+    gather<N, MODE, true>(a, k, g, p, lane, v, attempts, first, last, st_first, st_last);
     const V16 o = sum_round<N>(v);
     if (k.active && lane == 0) {
         write_log(a, k, g, log_word(attempts, first, last));
         a.consumed[static_cast<size_t>(p) * geo.w_max + k.c] = g;
     }
+    if (a.stamp_log && k.active && lane < N) write_stamp_log<N>(a, k, g, lane, st_first, st_last);
     if (!EPI) {
         if (k.lane_ok) st16(a.out + k.row, o);
         return;
@@ -777,7 +821,9 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
         if (EPI) rv = ld16(a.residual + k.row);  // this wave's own previous store
         V16 v[N];
         uint32_t attempts, first, last;
-        gather_chain<N>(a, k, g, p, lane, m_next, v, attempts, first, last, local);
+        const uint32_t st_first = st_next;
+        uint32_t st_last = st_next;
+        gather_chain<N>(a, k, g, p, lane, m_next, st_last, v, attempts, first, last, local);
         uint32_t *consumed = a.consumed + static_cast<size_t>(p) * geo.w_max + k.c;
         bool stop = false;
         // Once the payload has arrived: note the error word read with this
@@ -807,6 +853,8 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
             poll_next_and_release();
         }
         write_log(a, k, g, log_word(attempts, first, last));  // wave-uniform word
+        // lanes >= N store rank N - 1's stamps again: the same words to the same place
+        write_stamp_log<N>(a, k, g, lane < N ? lane : N - 1, st_first, st_last);
         const uint64_t ring = static_cast<uint64_t>(i) * A.ring_stride;
         if (!EPI) {
             // Lanes past the end of the row loaded the row's last 8 elements

@@ -55,22 +55,28 @@ struct ProduceArgs {
     int32_t entries;             // epoch g uses entry (g - 1) % entries
     const uint16_t *inject;      // [inject_entries] late | withheld << 8, or null
     int32_t inject_entries;
+    uint16_t *stage;             // [N][2][slot_elems], or null: with deterministic injection a
+                                 // late rank's payload is written here, not into its slot, and
+                                 // the reduction moves it into the slot when the rank catches up
     uint32_t *err;
 };
 
 struct ReduceArgs {
     Geometry geo;
     EpochRef ep;
-    const uint16_t *slots;
+    uint16_t *slots;             // written only when a late rank catches up (deterministic injection)
     uint32_t *stamps;
     uint32_t *consumed;
     uint32_t *log;               // [log_epochs][w_max]
+    uint32_t *stamp_log;         // [log_epochs][w_max][2][N]: the raw stamps of the chunk's first
+                                 // and last validation (per-epoch launches: may be null)
     int32_t log_epochs;
     uint32_t max_attempts;
     uint32_t forced_retries;
     uint32_t spin_limit;
     const uint16_t *inject;
     int32_t inject_entries;
+    const uint16_t *stage;       // late ranks' payload (ProduceArgs::stage), or null
     uint16_t *out;               // plain: [tokens][hidden]
     uint16_t *residual;          // epilogue: [tokens][hidden], in place
     const uint16_t *weight;      // [hidden]

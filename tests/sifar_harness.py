@@ -76,3 +76,42 @@ class StepRun:
         self.s.step(tokens)
         g1, _ = self.s.epochs()
         return list(range(g1 - self.L, g1))
+
+
+def read_stamp_log(s: "S.Sifar") -> np.ndarray:
+    """The raw-stamp log as [log_epochs][w_max][2][N]: rank r's stamp at a
+    chunk's first (index 0) and last (index 1) validation."""
+    epochs, _, w_max = s.log_geometry()
+    return s.read_stamp_log().reshape(epochs, w_max, 2, s.cfg.nranks)
+
+
+def stale_mask(stamps: np.ndarray, g: int) -> np.ndarray:
+    """Stale-rank masks recomputed from raw stamps [..., N] for epoch g."""
+    N = stamps.shape[-1]
+    bits = (stamps != (g & 0xFFFFFFFF)).astype(np.uint32) << np.arange(N, dtype=np.uint32)
+    return bits.sum(axis=-1).astype(np.uint32)
+
+
+def replay_logs(log: np.ndarray, stamp_log: np.ndarray, epochs, chunks: int):
+    """Replay every logged decision from the stamps logged with it: the first
+    and last stale-rank masks of each chunk's word must be the ones its
+    first and last stamps imply, and a chunk is accepted (last mask 0) only
+    when every stamp it validated against was fresh. Every stale stamp must be
+    an earlier epoch of the same slot parity (g - 2k) or the initial 0.
+    Returns (words checked, chunks that needed more than one validation)."""
+    checked = retried = 0
+    for g in epochs:
+        row = (g - 1) % log.shape[0]
+        words = log[row, :chunks]
+        st = stamp_log[row, :chunks]
+        first = stale_mask(st[:, 0], g)
+        last = stale_mask(st[:, 1], g)
+        assert np.array_equal((words >> 16) & 0xFF, first), f"epoch {g}: first masks"
+        assert np.array_equal(words >> 24, last), f"epoch {g}: last masks"
+        assert np.all(last == 0), f"epoch {g}: a chunk was accepted with a stale stamp"
+        stale = st[st != g].astype(np.int64)
+        assert np.all((stale == 0) | (((g - stale) % 2 == 0) & (stale < g))), \
+            f"epoch {g}: a stale stamp that is not an earlier epoch of the slot"
+        checked += chunks
+        retried += int(np.count_nonzero((words & 0xFFFF) > 1))
+    return checked, retried

@@ -18,8 +18,8 @@ from oracle import ref_np, sim
 
 pytestmark = pytest.mark.gpu
 
-from sifar_harness import (DEV, StepRun, expected_log_words, inject_table, to_dev, to_host,
-                           ulp_distance)
+from sifar_harness import (DEV, StepRun, expected_log_words, inject_table, read_stamp_log,
+                           replay_logs, to_dev, to_host, ulp_distance)
 
 ORDERS = {"spec": "spec", "ordered": "ordered"}
 
@@ -152,6 +152,54 @@ def test_stale_injection_deterministic(order, forced, fuse):
     assert int(np.count_nonzero(late)) > 0
     run.s.check()
     run.s.close()
+
+
+def test_spec_stress_full_length():
+    """The speculation stress workload at its stated length: N = 8, 4 tokens,
+    64 all-reduces per step, 200 steps, each rank's stamp late with p = 0.1.
+    Per-epoch launches with the peers fused into the reduction's launch, the
+    paper's speculative reduction. A late rank's payload waits in the stage
+    and its slot still holds its previous epoch when the reduction first loads
+    it, so only a retry that reloads the payload gets the sum right. Every
+    output of every step equals the no-speculation oracle, every decision-log
+    word equals the simulator's prediction, and every logged mask is the one
+    the logged raw stamps imply (on-time ranks fresh at the first validation,
+    late ranks holding the slot's previous epoch)."""
+    w = synth.SPEC_STRESS
+    steps, T, segs = w.steps, 4, 8
+    late = synth.delay_table(w.wid, w.nranks, w.reduces_per_step * steps, w.stale_prob)
+    run = StepRun(w, T, validate="spec", fuse_peers=1)
+    run.s.set_injection(inject_table(late))
+    retried = 0
+    for step in range(steps):
+        if step % 50 == 0:
+            print(f"spec stress step {step} of {steps}", flush=True)
+        epochs = run.step(T)
+        got = to_host(run.out_d)
+        exp = oracle.reduce_chain(run.pool, epochs, T)
+        for i in range(w.reduces_per_step):
+            assert np.array_equal(got[i, :T], exp[i]), f"step={step} node={i}"
+        log = run.s.read_log()
+        masks = [int(late[(g - 1) % len(late)]) for g in epochs]
+        pred = expected_log_words(w.nranks, masks, "spec", 0)
+        for i, g in enumerate(epochs):
+            row = log[(g - 1) % log.shape[0], :T * segs]
+            assert np.all(row == pred[i]), (step, i, hex(int(row[0])), hex(pred[i]))
+        st = read_stamp_log(run.s)
+        _, r = replay_logs(log, st, epochs, T * segs)
+        retried += r
+        for i, g in enumerate(epochs):
+            first = st[(g - 1) % st.shape[0], :T * segs, 0]
+            for rank in range(w.nranks):
+                if (masks[i] >> rank) & 1:
+                    assert np.all((first[:, rank] == g - 2) | (first[:, rank] == 0)), (g, rank)
+                else:
+                    assert np.all(first[:, rank] == g), (g, rank)
+    run.s.check()
+    run.s.close()
+    frac = retried / (steps * w.reduces_per_step * T * segs)
+    print(f"spec stress: {retried} chunk validations retried ({frac:.3f} of all)")
+    assert retried > 0
 
 
 def test_withheld_stamp_exhausts_budget():
@@ -584,6 +632,71 @@ def test_persistent_epilogue_moe_chain(T):
         res = r_list[-1]
     run.s.check()
     run.s.close()
+
+
+@pytest.mark.parametrize("T,steps", [(1, 100), (8, 10), (32, 3)])
+def test_persistent_epilogue_moe_chain_late_stamps(T, steps):
+    """The large-MoE workload as the persistent step runs it: N = 8, hidden
+    8192, 120 all-reduces per step, each followed by residual-add + RMSNorm,
+    each rank's stamp late (it lands late_delay sleeps after its payload) with
+    p = 0.05. After every step the residual stream is bit-exact and every y
+    within 1 bf16 step of the oracle; every chunk's decision word ends with a
+    clean validation, and every logged mask is the one the logged raw stamps
+    imply. Reports how many y elements sit 1 step away."""
+    w = synth.MOE_DECODE
+    late = synth.delay_table(w.wid, w.nranks, w.reduces_per_step * steps, w.stale_prob)
+    run = StepRun(w, 32, persistent=1, late_delay=8)
+    run.s.set_injection(inject_table(late))
+    res = run.res0[:T].copy()
+    segs = 16
+    off_by_one = total = retried = 0
+    for step in range(steps):
+        if step % 10 == 0:
+            print(f"persistent moe late stamps T={T} step {step} of {steps}", flush=True)
+        epochs = run.step(T)
+        y_got = to_host(run.y_d[:, :T])
+        _, r_list, y_list = oracle.reduce_chain(run.pool, epochs, T,
+                                                epilogue=(res, run.weight, w.rms_eps))
+        assert np.array_equal(to_host(run.res_d)[:T], r_list[-1]), f"step {step}: residual"
+        for i in range(w.reduces_per_step):
+            d = ulp_distance(y_got[i, :T], y_list[i])
+            assert d.max() <= 1, f"step {step} node {i}: y off by {d.max()} steps"
+            off_by_one += int(np.count_nonzero(d))
+            total += d.size
+        res = r_list[-1]
+        log = run.s.read_log()
+        _, r = replay_logs(log, read_stamp_log(run.s), epochs, T * segs)
+        retried += r
+    run.s.check()
+    run.s.close()
+    print(f"persistent moe T={T}: {off_by_one} of {total} y elements 1 bf16 step from the "
+          f"oracle ({off_by_one / total:.2e}); {retried} chunk validations polled again")
+    assert retried > 0
+
+
+@pytest.mark.parametrize("T", [4, 8])
+def test_persistent_late_stamps_log_replay(T):
+    """Free-running persistent steps with late stamps: each decision word is
+    replayed from the raw stamps logged with it."""
+    w = synth.SPEC_STRESS
+    steps = 20
+    late = synth.delay_table(w.wid, w.nranks, w.reduces_per_step * steps, w.stale_prob)
+    run = StepRun(w, T, persistent=1, late_delay=4)
+    run.s.set_injection(inject_table(late))
+    checked = retried = 0
+    for step in range(steps):
+        epochs = run.step(T)
+        got = to_host(run.out_d)
+        for i in range(0, w.reduces_per_step, 9):
+            g = epochs[i]
+            assert np.array_equal(got[i, :T], oracle.reduce(run.pool[(g - 1) % run.pool.shape[0]][:, :T]))
+        c, r = replay_logs(run.s.read_log(), read_stamp_log(run.s), epochs, T * 8)
+        checked += c
+        retried += r
+    run.s.check()
+    run.s.close()
+    print(f"log replay T={T}: {checked} words, {retried} polled more than once")
+    assert retried > 0
 
 
 @pytest.mark.parametrize("N,T,H", [(5, 16, 3896), (8, 8, 4608), (3, 32, 2048),
