@@ -8,16 +8,24 @@ chained all-reduces per decode step (32 layers x 2). Synthetic activations
 N(0,1)*0.5 with 0.1 % outliers x50, seeded. Inputs are resident in HBM before
 timing starts.
 
-One benchmark step = one captured decode step (64 x produce + reduce, plus
-the epoch advance) for each of the four batch sizes: 256 all-reduces.
+One benchmark step = one decode step of 64 all-reduces for each of the four
+batch sizes: 256 all-reduces. By default (--persistent 1) a decode step is one
+persistent kernel launch whose consumer waves poll the stamps before they load
+the payload (ORDERED: no speculation) while producer waves play the peers
+concurrently; --persistent 0 replays a captured graph with one launch per
+all-reduce, whose reduction is the paper's speculative one (SPEC).
 
 Printed JSON line (rank 0):
   value            microseconds per all-reduce over the timed steps (HIP events
-                   around the graph replays; includes the emulated peers'
+                   around the step launches; includes the emulated peers'
                    writes and every dispatch gap)
-  roofline         the reduction kernel: algorithmic bytes per launch over its
-                   average launch duration, from HIP events around each launch
-                   on the launching stream
+  roofline         the dominant kernel: one consumer's algorithmic bytes per
+                   launch (read N*K, write K, stamps; the emulated peers'
+                   copies are reported apart) over its average launch period,
+                   from HIP events on the launching stream; frac_cold the same
+                   for steps run right after a 512 MiB scrub of the caches
+  spec_graph       the speculative per-launch chain on the same workload, with
+                   its own dominant kernel's fraction
   cpu_baseline     the CPU oracle on this host, on a bounded sample
 """
 from __future__ import annotations
@@ -42,6 +50,12 @@ def reduce_bytes(N: int, T: int, H: int) -> int:
     K = T * H * 2
     chunks = T * ((H + 511) // 512)
     return N * K + K + 4 * N * chunks
+
+
+def epilogue_bytes(T: int, H: int) -> int:
+    """Extra algorithmic bytes of the fused residual-add + RMSNorm: read and
+    write the residual, write y (K each), read the weight (2H)."""
+    return 3 * T * H * 2 + 2 * H
 
 
 def produce_bytes(N: int, T: int, H: int) -> int:
@@ -183,6 +197,8 @@ def parse():
                     help="reduce-cold: waves per workgroup of the reduction kernel")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline (0 disables it)")
+    ap.add_argument("--spec-graph", type=int, default=1,
+                    help="persistent runs: also time the speculative per-launch chain (1)")
     ap.add_argument("--wide-points", type=int, default=1,
                     help="also time the chain at 16 and 64 tokens (1) or not (0: profiling "
                          "runs, whose averages cover the headline launches only)")
@@ -218,49 +234,26 @@ def cpu_baseline(pool, tokens, budget_s):
 
 
 def cpu_baseline_parallel(pool, tokens, budget_s, threads):
-    """The same C oracle entry point driven from up to `threads` host threads,
-    each reducing one contiguous slice of the T x H elements in place (the
-    oracle takes the rank stride and the element count separately). Slices
-    hold at least 8192 elements: a Python thread hand-off costs tens of
-    microseconds, more than a smaller slice's work. Checked once against the
-    single-threaded call."""
-    from concurrent.futures import ThreadPoolExecutor
-
+    """The same C oracle on `threads` native host threads (oracle's pthread
+    driver: each thread runs the oracle's reduction on a contiguous slice of
+    the T x H elements; bit-identical, checked once against the
+    single-threaded call)."""
     import numpy as np
     import oracle
 
-    lib = oracle.lib()
     per_t = {}
-    with ThreadPoolExecutor(threads) as ex:
-        for T in tokens:
-            xs = [np.ascontiguousarray(pool[e][:, :T]) for e in range(8)]
-            outs = [np.empty(x.shape[1:], np.uint16) for x in xs]
-            n_ranks, count = xs[0].shape[0], xs[0][0].size
-            parts = max(1, min(threads, count // 8192))
-            cuts = np.linspace(0, count, parts + 1).astype(np.int64)
-            spans = [(int(a), int(b)) for a, b in zip(cuts[:-1], cuts[1:]) if b > a]
-
-            def reduce_all(x, o):
-                def one(span):
-                    i0, i1 = span
-                    lib.oracle_reduce(x.ctypes.data + 2 * i0, n_ranks, count, i1 - i0,
-                                      o.ctypes.data + 2 * i0)
-                if len(spans) == 1:
-                    one(spans[0])
-                else:
-                    list(ex.map(one, spans))
-
-            reduce_all(xs[0], outs[0])
-            assert np.array_equal(outs[0], oracle.reduce(xs[0]))
-            n, t0 = 0, time.perf_counter()
-            while True:
-                reduce_all(xs[n % len(xs)], outs[n % len(xs)])
-                n += 1
-                el = time.perf_counter() - t0
-                if el > budget_s / len(tokens):
-                    break
-            per_t[T] = (el / n * 1e6, len(spans))
-    return sum(v for v, _ in per_t.values()) / len(per_t), per_t
+    for T in tokens:
+        xs = [np.ascontiguousarray(pool[e][:, :T]) for e in range(8)]
+        assert np.array_equal(oracle.reduce_threads(xs[0], threads), oracle.reduce(xs[0]))
+        n, t0 = 0, time.perf_counter()
+        while True:
+            oracle.reduce_threads(xs[n % len(xs)], threads)
+            n += 1
+            el = time.perf_counter() - t0
+            if el > budget_s / len(tokens):
+                break
+        per_t[T] = el / n * 1e6
+    return sum(per_t.values()) / len(per_t), per_t
 
 
 def host_cpu() -> str:
@@ -351,22 +344,44 @@ def chain_point(w, T, args, *, T_max=None, pool_entries=None, inject=False, wave
     fused_launch = args.fuse and args.buffers == 2
     launches = 1 if args.persistent else (L + 2 if fused_launch else 2 * L + 1)
     out["launch_period_us"] = ms * 1e3 / (args.steps * launches)
-    K = T * H * 2
-    red = reduce_bytes(N, T, H) + (3 * K + 2 * H if w.epilogue else 0)
+    red = reduce_bytes(N, T, H) + (epilogue_bytes(T, H) if w.epilogue else 0)
     out["reduce_bytes"] = red
     out["reduce_gbs"] = red / (out["us_per_reduce"] * 1e-6) / 1e9
-    fused = red + (produce_bytes(N, T, H) if (fused_launch or args.persistent) else 0)
-    if args.persistent:
-        fused *= L
-    out["launch_bytes"] = fused
-    out["launch_gbs"] = fused / (out["launch_period_us"] * 1e-6) / 1e9
-    # parity spot check of the last replay (outside the timed region)
+    peers = produce_bytes(N, T, H) if (fused_launch or args.persistent) else 0
+    per_launch = L if args.persistent else 1
+    out["launch_bytes"] = red * per_launch
+    out["launch_gbs"] = red * per_launch / (out["launch_period_us"] * 1e-6) / 1e9
+    out["peer_copy_bytes_per_launch"] = peers * per_launch
+    # parity check of the last replay (outside the timed region)
     got = ring.cpu().numpy().view(np.uint16)
     if not w.epilogue:
         for i in check_nodes:
             g = epochs[i]
             exp = oracle.reduce(pool[(g - 1) % P][:, :T])
             assert np.array_equal(got[i, :T], exp), f"{w.name} T={T} node {i}"
+    else:
+        # one more step, untimed, from a known residual: the residual after it
+        # bit-exact, every node's y within 1 bf16 step
+        res_before = res_d.cpu().numpy().view(np.uint16)[:T].copy()
+        s.step(T, stream)
+        torch.cuda.synchronize()
+        s.check()
+        nxt, _ = s.epochs()
+        epochs = list(range(nxt - L, nxt))
+        _, r_list, y_list = oracle.reduce_chain(pool, epochs, T,
+                                                epilogue=(res_before, wgt, w.rms_eps))
+        assert np.array_equal(res_d.cpu().numpy().view(np.uint16)[:T], r_list[-1]), \
+            f"{w.name} T={T}: residual"
+        y_got = ring[:, :T].cpu().numpy().view(np.uint16)
+        key = lambda x: np.where(x.astype(np.int32) & 0x8000, -(x.astype(np.int32) & 0x7FFF),
+                                 x.astype(np.int32))
+        off = 0
+        for i in range(L):
+            d = np.abs(key(y_got[i]) - key(y_list[i]))
+            assert d.max() <= 1, f"{w.name} T={T} node {i}: y off by {d.max()}"
+            off += int(np.count_nonzero(d))
+        out["y_elements_one_step_off"] = off
+        out["y_elements_checked"] = L * T * H
     log = s.read_log()
     segs = (H + 511) // 512
     rows = np.array([log[(g - 1) % L, :T * segs] for g in epochs])
@@ -384,6 +399,73 @@ def chain_point(w, T, args, *, T_max=None, pool_entries=None, inject=False, wave
             out["log_matches_prediction"] = True
     s.close()
     return out
+
+
+def kernel_table(per_t, tokens, N, H, L, persistent, fused_launch):
+    """Per batch size: the dominant kernel's launch period (from the HIP-event
+    microseconds per all-reduce of a step), one consumer's algorithmic bytes
+    per launch and the emulated peers' copy bytes per launch."""
+    if persistent:
+        launches, per_launch = 1, L
+    else:
+        launches, per_launch = (L + 2 if fused_launch else 2 * L + 1), 1
+    kern = {}
+    for T in tokens:
+        period_us = per_t[T] * L / launches
+        byts = per_launch * reduce_bytes(N, T, H)
+        peers = per_launch * produce_bytes(N, T, H) if (fused_launch or persistent) else 0
+        kern[T] = {"launch_period_us": period_us, "bytes_per_launch": byts,
+                   "gbs": byts / (period_us * 1e-6) / 1e9,
+                   "peer_copy_bytes_per_launch": peers}
+    return kern
+
+
+def spec_graph_point(w, pool, pool_d, args):
+    """The paper's speculative reduction on the headline workload: one
+    captured graph per decode step with one launch per all-reduce (the peers
+    of epoch g + 1 written by a second plane of the launch that reduces g),
+    payload and stamps loaded together, validated afterwards. Timed like the
+    headline (HIP events around the graph replays); its dominant kernel is the
+    fused reduction, L - 1 of a step's L + 2 launches. The last replay's
+    outputs are checked against the oracle."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2607_08973_amd as S
+
+    N, H, L, tokens = w.nranks, w.hidden, w.reduces_per_step, w.tokens
+    T_max = max(tokens)
+    ring = torch.zeros((L, T_max, H), dtype=torch.int16, device="cuda:0")
+    stream = torch.cuda.current_stream()
+    s = S.Sifar(nranks=N, hidden=H, max_tokens=T_max, reduces_per_step=L, validate="spec",
+                log_epochs=L, fuse_peers=1, persistent=0)
+    s.bind_step(pool_d, out_ring=ring)
+    per_t = {}
+    for T in tokens:
+        for _ in range(args.warmup):
+            s.step(T, stream)
+        per_t[T] = time_steps(s, T, args.steps, stream) * 1e3 / (args.steps * L)
+        s.check()
+        nxt, _ = s.epochs()
+        got = ring.cpu().numpy().view(np.uint16)
+        for i in (0, L // 2, L - 1):
+            g = nxt - L + i
+            assert np.array_equal(got[i, :T], oracle.reduce(pool[(g - 1) % pool.shape[0]][:, :T])), \
+                f"spec graph T={T} node {i}"
+    s.close()
+    kern = kernel_table(per_t, tokens, N, H, L, False, True)
+    period = sum(k["launch_period_us"] for k in kern.values()) / len(kern)
+    byts = sum(k["bytes_per_launch"] for k in kern.values()) / len(kern)
+    gbs = byts / (period * 1e-6) / 1e9
+    return {"protocol": "SPEC: payload and stamps loaded together, validated after, retried "
+                        "on a stale stamp; one graph launch per all-reduce",
+            "us_per_reduce": round(sum(per_t.values()) / len(per_t), 4),
+            "us_per_reduce_by_tokens": {str(k): round(v, 4) for k, v in per_t.items()},
+            "dominant_kernel": "reduce_kernel<8, SPEC, no epilogue, fused peers>",
+            "launch_period_us": round(period, 4), "bytes_per_launch": round(byts),
+            "achieved_gbs": round(gbs, 3), "frac": round(gbs / HBM_PEAK_GBS, 6),
+            "traffic": measured_traffic("fused")}
 
 
 def reduce_point(w, args, scrub, reps=30):
@@ -482,6 +564,7 @@ def suite(args):
         import paper_2607_08973_amd as S
         trials = 65536
         for proto, pname in ((S.SIFAR_LITMUS_ORDERED, "ordered"),
+                             (S.SIFAR_LITMUS_ORDERED_PREFETCH, "ordered-prefetching-producer"),
                              (S.SIFAR_LITMUS_READ_FIRST, "read-first")):
             for place, lname in ((S.SIFAR_LITMUS_CROSS_XCD, "cross-xcd"),
                                  (S.SIFAR_LITMUS_SAME_XCD, "same-xcd")):
@@ -642,8 +725,6 @@ def main():
         torch.cuda.synchronize()
         per_t[T] = a.elapsed_time(b) * 1e3 / (args.steps * L)
     s.check()
-    graph_next_epoch, _ = s.epochs()   # the ring now holds the last step at T = tokens[-1]
-    graph_ring = ring.cpu().numpy().view(np.uint16).copy()
 
     # ---- the metric's larger batch sizes, outside the timed region ---------
     # The metric spans 1-64 tokens; the workload's batch sizes stop at 8. The
@@ -663,25 +744,49 @@ def main():
     floors = latency_floors()
 
     # ---- roofline of the dominant kernel -----------------------------------
-    # With fused peers a step is produce(g1), L-1 launches of the fused
+    # Persistent: one launch per step, L all-reduces in it. Per launch: with
+    # fused peers a step is produce(g1), L-1 launches of the fused
     # reduce(g_i)+produce(g_i+1) kernel, reduce(g_L) and the epoch advance:
-    # the fused kernel is L-1 of the L+2 launches. Its average launch period
+    # the fused kernel is L-1 of the L+2 launches; its average launch period
     # is the HIP-event step time over the launches of the step.
-    fused_launch = args.fuse and args.buffers == 2
-    if args.persistent:
-        launches, per_launch = 1, L
-    else:
-        launches, per_launch = (L + 2 if fused_launch else 2 * L + 1), 1
-    kern = {}
-    for T in tokens:
-        period_us = per_t[T] * L / launches
-        byts = per_launch * (reduce_bytes(N, T, H) +
-                             (produce_bytes(N, T, H) if (fused_launch or args.persistent) else 0))
-        kern[T] = {"launch_period_us": period_us, "bytes_per_launch": byts,
-                   "gbs": byts / (period_us * 1e-6) / 1e9}
+    # Algorithmic bytes are one consumer's share of each all-reduce (read
+    # N*K, write K, read the stamps); the emulated peers' copies (read N*K,
+    # write N*K, write the stamps) are reported apart.
+    kern = kernel_table(per_t, tokens, N, H, L, args.persistent, args.fuse and args.buffers == 2)
     mean_period = sum(k["launch_period_us"] for k in kern.values()) / len(kern)
     mean_bytes = sum(k["bytes_per_launch"] for k in kern.values()) / len(kern)
+    mean_peer = sum(k["peer_copy_bytes_per_launch"] for k in kern.values()) / len(kern)
     achieved = mean_bytes / (mean_period * 1e-6) / 1e9
+
+    # ---- the same steps cold: a 512 MiB write before each step ------------
+    # pushes the pool, the slots and the outputs out of the L2s and the
+    # Infinity Cache; HIP events bracket the step alone.
+    scrub = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    cold_t = {}
+    for T in tokens:
+        reps, tot = 10, 0.0
+        for k in range(reps):
+            scrub.fill_(k & 0x7F)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            s.step(T, stream)
+            b.record(stream)
+            torch.cuda.synchronize()
+            tot += a.elapsed_time(b) * 1e3
+        cold_t[T] = tot / (reps * L)
+    s.check()
+    kern_cold = kernel_table(cold_t, tokens, N, H, L, args.persistent,
+                             args.fuse and args.buffers == 2)
+    cold_period = sum(k["launch_period_us"] for k in kern_cold.values()) / len(kern_cold)
+    achieved_cold = mean_bytes / (cold_period * 1e-6) / 1e9
+    del scrub
+    graph_next_epoch, _ = s.epochs()   # the ring now holds the last step at T = tokens[-1]
+    graph_ring = ring.cpu().numpy().view(np.uint16).copy()
+
+    # ---- the speculative per-launch chain (the paper's SPEC) --------------
+    spec = None
+    if args.persistent and args.spec_graph:
+        spec = spec_graph_point(w, pool, pool_d, args)
 
     # ---- parity spot check of the timed graph (outside the timed region) --
     import oracle
@@ -719,17 +824,14 @@ def main():
             avail = len(os.sched_getaffinity(0))
         except (AttributeError, OSError):
             avail = os.cpu_count() or 1
-        threads = max(1, min(avail, int(os.environ.get("OMP_NUM_THREADS", "16")), 16))
+        threads = max(1, avail)
         par_us, par_t = cpu_baseline_parallel(pool, tokens, args.cpu_seconds / 3, threads)
         cpu["parallel"] = {
-            "value": round(par_us, 3), "unit": "us per all-reduce",
-            "cores": max(k for _, k in par_t.values()),
-            "sample": f"the same oracle entry point on up to {threads} threads (cores = the "
-                      f"most it used), each a "
-                      f"contiguous slice of at least 8192 of the T x H elements, "
+            "value": round(par_us, 3), "unit": "us per all-reduce", "cores": threads,
+            "sample": f"the same oracle reduction on {threads} native threads (every core this "
+                      f"process may use), each a contiguous slice of the T x H elements, "
                       f"{args.cpu_seconds / 3:.0f} s total: " +
-                      ", ".join(f"T={t}: {v:.1f} us on {k} thread(s)"
-                                for t, (v, k) in par_t.items())}
+                      ", ".join(f"T={t}: {v:.1f} us" for t, v in par_t.items())}
 
     s.close()
     rec = {
@@ -747,6 +849,10 @@ def main():
         "data": "synthetic (seeded N(0,1)*0.5 activations, 0.1% outliers x50)",
         "config": {"workload": w.name, "nranks": N, "hidden": H, "tokens": list(tokens),
                    "reduces_per_step": L, "validate": args.mode, "fuse_peers": args.fuse,
+                   "protocol": ("ORDERED: stamps polled before the payload is loaded (no "
+                                "speculation), peers concurrent in one persistent launch"
+                                if args.persistent else
+                                f"{args.mode.upper()} in one launch per all-reduce"),
                    "persistent": args.persistent, "buffers": args.buffers,
                    "step": (f"{len(tokens)} decode steps of {L} all-reduces, one persistent "
                             f"launch each" if args.persistent else
@@ -761,10 +867,20 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
                      "traffic": traffic, "bytes_per_launch": round(mean_bytes),
+                     "bytes": "one consumer's share per all-reduce: read N*K, write K, "
+                              "4*N bytes of stamps per 512-element chunk; times the "
+                              "all-reduces per launch",
                      "residency": "warm: each epoch's slots were just written by the same "
-                                  "step's producer waves (cold reduction rates: "
-                                  "--workload reduce-cold)",
-                     "launch_period_us": round(mean_period, 4)},
+                                  "step's producer waves",
+                     "launch_period_us": round(mean_period, 4),
+                     "frac_cold": round(achieved_cold / HBM_PEAK_GBS, 6),
+                     "launch_period_cold_us": round(cold_period, 4),
+                     "cold": "the same steps, each right after a 512 MiB write that pushes "
+                             "the source pool, slots and outputs out of the L2s and the "
+                             "Infinity Cache; HIP events around the step alone",
+                     "peer_copy_bytes_per_launch": round(mean_peer),
+                     "peer_copy_gbs": round(mean_peer / (mean_period * 1e-6) / 1e9, 3)},
+        "spec_graph": spec,
         "cpu_baseline": cpu,
         "wall_s_timed": round(wall, 3),
     }

@@ -13,6 +13,9 @@ Contents
              cross-checked against ref.c
   sim.py     a deterministic interleaving simulator of the stamp / validate /
              retry protocol (Sec. 4.1-4.2, correctness argument of Sec. 8.1)
+  par.c      a host-thread driver of ref.c's reduction over slices of the
+             elements (no arithmetic of its own), for the benchmark's
+             multi-core CPU baseline
 
 This module wraps ref.c through ctypes. ``build()`` compiles it with gcc.
 """
@@ -26,6 +29,7 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "ref.c")
+PAR = os.path.join(HERE, "par.c")
 LIB = os.path.join(HERE, "libsifar_oracle.so")
 CFLAGS = ["-O2", "-fno-fast-math", "-ffp-contract=off", "-fPIC", "-shared", "-std=c11"]
 
@@ -36,7 +40,7 @@ def build(force: bool = True) -> str:
     """Compile ref.c into libsifar_oracle.so (always, unless force=False and it exists)."""
     if force or not os.path.exists(LIB):
         tmp = LIB + ".tmp"
-        subprocess.run(["gcc", *CFLAGS, SRC, "-o", tmp, "-lm"], check=True)
+        subprocess.run(["gcc", *CFLAGS, SRC, PAR, "-o", tmp, "-lm", "-lpthread"], check=True)
         os.replace(tmp, LIB)
     return LIB
 
@@ -64,6 +68,9 @@ def lib():
         L.oracle_bf16_value_array.argtypes = [ctypes.c_void_p, ctypes.c_size_t,
                                               ctypes.c_void_p]
         L.oracle_bf16_value_array.restype = None
+        L.oracle_reduce_threads.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t,
+                                            ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int]
+        L.oracle_reduce_threads.restype = ctypes.c_int
         L.oracle_fp_env_ok.argtypes = []
         L.oracle_fp_env_ok.restype = ctypes.c_int
         _lib = L
@@ -107,6 +114,19 @@ def reduce(x: np.ndarray) -> np.ndarray:
     count = x[0].size
     out = np.empty(x.shape[1:], dtype=np.uint16)
     lib().oracle_reduce(_ptr(x), n, count, count, _ptr(out))
+    return out
+
+
+def reduce_threads(x: np.ndarray, threads: int) -> np.ndarray:
+    """``reduce`` computed by ``threads`` host threads, each running the same
+    C reduction on a contiguous slice of the elements (bit-identical)."""
+    x = np.ascontiguousarray(x, dtype=np.uint16)
+    n = x.shape[0]
+    count = x[0].size
+    out = np.empty(x.shape[1:], dtype=np.uint16)
+    used = lib().oracle_reduce_threads(_ptr(x), n, count, count, _ptr(out), int(threads))
+    if used < 0:
+        raise RuntimeError("oracle_reduce_threads could not start its threads")
     return out
 
 

@@ -361,3 +361,14 @@ def test_reduce_chain_uses_pool_entries_cyclically():
     for g, o in zip(range(1, 10), outs):
         assert np.array_equal(o, oracle.reduce(pool[(g - 1) % 4][:, :1, :]))
     assert np.array_equal(outs[0], outs[4])
+
+
+def test_threaded_driver_is_bit_identical():
+    """The benchmark's multi-core CPU baseline runs the oracle's reduction on
+    slices from native threads: same bits as one call, for any thread count,
+    including more threads than elements."""
+    import synth
+    x = synth.payload_pool(2, 8, 3, 1000, 1, "act")[0]
+    want = oracle.reduce(x)
+    for threads in (1, 2, 7, 16, 5000):
+        assert np.array_equal(oracle.reduce_threads(x, threads), want), threads
