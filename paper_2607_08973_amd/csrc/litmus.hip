@@ -12,6 +12,13 @@
 //  - READ_FIRST, the paper's speculative order (Sec. 4.2): load payload and
 //    stamps together, accept when every stamp is fresh, else acquire and
 //    reload both.
+// Two producer forms: the plain one stores the slot and waits for every
+// outstanding operation (publish_slot); the prefetching one publishes as the
+// persistent step's prefetching producer does -- buffer stores of the slot,
+// then buffer loads of the next epoch's sources, then a wait until at most
+// those loads are outstanding (vmcnt(8)), then the flags -- so the ordering
+// that wait relies on (one wave's vector memory operations leave the counter
+// in issue order) is checked on the sequence the benchmark's kernel runs.
 // Pairs are laid out so that, with workgroups dealt to the XCDs round robin,
 // producer and consumer sit on different XCDs (or on the same one); each wave
 // reads its XCC_ID and the pair reports whether it landed as intended, and the
@@ -50,7 +57,8 @@ struct LitmusArgs {
     uint64_t *place;     // [producer, consumer][pair]
     uint32_t *out;       // [pair][O_WORDS]
     uint64_t *ticks;     // [pair][2]: consumer's start and end
-    int pairs, trials, read_first, cross;
+    const uint32_t *src; // [pair][rank][lane][4], all zero: the prefetching producer's sources
+    int pairs, trials, read_first, cross, prefetch;
 };
 
 // Word w of rank r and lane l in epoch g.
@@ -64,9 +72,67 @@ __device__ __forceinline__ uint32_t *slot_of(const LitmusArgs &a, int pair, uint
            lane * 4;
 }
 
+// Slot word offset of rank r's 16 bytes for `lane`, from the pair's parity-p
+// slot start (the buffer form's per-lane byte offset).
+__device__ __forceinline__ uint32_t lane_bytes(int lane) { return static_cast<uint32_t>(lane) * 16u; }
+
+// The prefetching producer: epoch g's slot is stored from values derived from
+// sources loaded one epoch earlier (zeros, unknown to the compiler), and the
+// next epoch's sources are loaded while the slot stores travel.
+__device__ void producer_prefetch(const LitmusArgs &a, int pair, int lane, bool local) {
+    const uint32_t *src = a.src + static_cast<size_t>(pair) * kLitmusRanks * kWaveLanes * 4;
+    V16 raw[kLitmusRanks];
+#pragma unroll
+    for (int r = 0; r < kLitmusRanks; ++r)
+        raw[r] = ld16_buffer<0>(src + r * kWaveLanes * 4, lane_bytes(lane));
+    for (int i = 1; i <= a.trials; ++i) {
+        const uint32_t g = static_cast<uint32_t>(i), p = g & 1u;
+        const size_t pc = static_cast<size_t>(p) * a.pairs + pair;
+        bool free = false;
+        for (uint32_t spins = 0; spins < kSpins; ++spins) {
+            free = ld_relaxed(a.consumed + pc) == ld_relaxed(a.produced + pc);
+            if (free) break;
+            __builtin_amdgcn_s_sleep(1);
+        }
+        if (!free) {
+            if (lane == 0) a.out[pair * O_WORDS + O_PRODUCER_TIMEOUT] = 1;
+            return;
+        }
+#pragma unroll
+        for (int r = 0; r < kLitmusRanks; ++r) {
+            V16 v;
+#pragma unroll
+            for (int w = 0; w < 4; ++w) v.w[w] = raw[r].w[w] + value_of(g, r, lane, w);
+            st16_buffer(slot_of(a, pair, p, r, 0), lane_bytes(lane), v);
+        }
+        if (local) {
+            // the loads stay after the stores (the wait below counts on it)
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);
+#pragma unroll
+            for (int r = 0; r < kLitmusRanks; ++r)
+                raw[r] = ld16_buffer<0>(src + r * kWaveLanes * 4, lane_bytes(lane));
+            // at most the 8 source loads outstanding: the slot stores have
+            // reached the L2
+            __builtin_amdgcn_s_waitcnt(kWaitVm | kLitmusRanks);
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        } else {
+#pragma unroll
+            for (int r = 0; r < kLitmusRanks; ++r)
+                raw[r] = ld16_buffer<0>(src + r * kWaveLanes * 4, lane_bytes(lane));
+            publish_slot(false);
+        }
+        if (lane < kLitmusRanks) st_flag(a.stamps + pc * kLitmusRanks + lane, g, local);
+        if (lane == 0) st_flag(a.produced + pc, g, local);
+    }
+}
+
 __device__ void producer(const LitmusArgs &a, int pair, int lane) {
     publish_place(a.place + pair, 0, lane);
     const bool local = partner_is_local(a.place + a.pairs + pair, 0, lane);
+    if (a.prefetch) {
+        producer_prefetch(a, pair, lane, local);
+        return;
+    }
     for (int i = 1; i <= a.trials; ++i) {
         const uint32_t g = static_cast<uint32_t>(i), p = g & 1u;
         const size_t pc = static_cast<size_t>(p) * a.pairs + pair;
@@ -224,7 +290,9 @@ extern "C" int sifar_litmus(int32_t protocol, int32_t placement, int32_t pairs, 
                             void *stream, sifar_litmus_result *result) {
     using namespace sifar;
     if (!result) return SIFAR_EINVAL;
-    if (protocol != SIFAR_LITMUS_ORDERED && protocol != SIFAR_LITMUS_READ_FIRST) return SIFAR_EINVAL;
+    if (protocol != SIFAR_LITMUS_ORDERED && protocol != SIFAR_LITMUS_READ_FIRST &&
+        protocol != SIFAR_LITMUS_ORDERED_PREFETCH)
+        return SIFAR_EINVAL;
     if (placement != SIFAR_LITMUS_CROSS_XCD && placement != SIFAR_LITMUS_SAME_XCD) return SIFAR_EINVAL;
     if (pairs < 8 || pairs > kMaxPairs || pairs % 8 != 0) return SIFAR_EINVAL;
     if (trials < 1 || trials > kMaxTrials) return SIFAR_EINVAL;
@@ -241,11 +309,14 @@ extern "C" int sifar_litmus(int32_t protocol, int32_t placement, int32_t pairs, 
                              static_cast<size_t>(pairs) * O_WORDS;
     const size_t ctl_bytes = ctl_words * sizeof(uint32_t) +
                              static_cast<size_t>(pairs) * 4 * sizeof(uint64_t);
-    Buffer slots, ctl;
+    const size_t src_bytes = static_cast<size_t>(pairs) * kSlotWords * sizeof(uint32_t);
+    Buffer slots, ctl, src;
     if (hipMalloc(&slots.p, slot_bytes) != hipSuccess) return SIFAR_ENOMEM;
     if (hipMalloc(&ctl.p, ctl_bytes) != hipSuccess) return SIFAR_ENOMEM;
+    if (hipMalloc(&src.p, src_bytes) != hipSuccess) return SIFAR_ENOMEM;
     rc = hip_rc(hipMemsetAsync(slots.p, 0, slot_bytes, s));
     if (!rc) rc = hip_rc(hipMemsetAsync(ctl.p, 0, ctl_bytes, s));
+    if (!rc) rc = hip_rc(hipMemsetAsync(src.p, 0, src_bytes, s));
     if (rc) return rc;
 
     LitmusArgs a{};
@@ -261,6 +332,8 @@ extern "C" int sifar_litmus(int32_t protocol, int32_t placement, int32_t pairs, 
     a.pairs = pairs;
     a.trials = trials;
     a.read_first = protocol == SIFAR_LITMUS_READ_FIRST;
+    a.prefetch = protocol == SIFAR_LITMUS_ORDERED_PREFETCH;
+    a.src = static_cast<const uint32_t *>(src.p);
     a.cross = placement == SIFAR_LITMUS_CROSS_XCD;
     hipLaunchKernelGGL(litmus_kernel, dim3(2 * pairs), dim3(kWaveLanes), 0, s, a);
     rc = hip_rc(hipGetLastError());

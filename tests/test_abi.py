@@ -119,7 +119,7 @@ def test_floor_rejects_bad_arguments_on_host(kind, iterations):
 
 
 @pytest.mark.parametrize("protocol,placement,pairs,trials", [
-    (2, 0, 8, 10), (-1, 0, 8, 10), (0, 2, 8, 10), (0, 0, 0, 10), (0, 0, 12, 10),
+    (3, 0, 8, 10), (-1, 0, 8, 10), (0, 2, 8, 10), (0, 0, 0, 10), (0, 0, 12, 10),
     (0, 0, 520, 10), (0, 0, 8, 0), (0, 0, 8, (1 << 20) + 1),
 ])
 def test_litmus_rejects_bad_arguments(protocol, placement, pairs, trials):

@@ -33,18 +33,37 @@ def test_ordered_handoff_never_stale(placement):
 
 
 @pytest.mark.parametrize("placement", [S.SIFAR_LITMUS_CROSS_XCD, S.SIFAR_LITMUS_SAME_XCD])
-def test_read_first_handoff(placement):
-    """The paper's read-first order against a live producer. Across XCDs it
-    accepts words of an earlier epoch (measured: about 0.2 % of the handoffs
-    with 256 pairs), which shows that the litmus sees the hazard the ORDERED
-    reader closes; on one XCD the rate is only reported."""
-    print(f"litmus read-first placement {placement} pairs {PAIRS} trials {TRIALS}", flush=True)
-    r = S.sifar_litmus(S.SIFAR_LITMUS_READ_FIRST, placement, PAIRS, TRIALS)
+def test_prefetching_publication_never_stale(placement):
+    """The persistent step's prefetching producer publishes a slot by waiting
+    until only the next epoch's source loads are outstanding (vmcnt(8)) before
+    it stores the flags on one XCD. With that exact sequence the ORDERED reader
+    must accept no stale word in 2.1 million handoffs per placement."""
+    print(f"litmus ordered-prefetch placement {placement} pairs {PAIRS} trials {TRIALS}",
+          flush=True)
+    r = S.sifar_litmus(S.SIFAR_LITMUS_ORDERED_PREFETCH, placement, PAIRS, TRIALS)
     print(r, flush=True)
     assert r["timeouts"] == 0
     assert r["trials"] == PAIRS * TRIALS
-    if placement == S.SIFAR_LITMUS_CROSS_XCD:
-        assert r["violations"] > 0
+    assert r["violations"] == 0, r["first_bad"]
+    assert r["pairs_placed"] == PAIRS
+
+
+@pytest.mark.parametrize("placement", [S.SIFAR_LITMUS_CROSS_XCD, S.SIFAR_LITMUS_SAME_XCD])
+def test_read_first_handoff(placement):
+    """The paper's read-first order against a live producer. Whether it
+    accepts a stale word depends on timing (the interleaving of the paper's
+    monotonicity discussion: the payload load served before the producer's
+    write arrives, the stamp load after its stamp), so the rate is reported,
+    not asserted; every violation found must be a word of an earlier epoch of
+    the same slot, or the slot's initial zeros."""
+    print(f"litmus read-first placement {placement} pairs {PAIRS} trials {TRIALS}", flush=True)
+    r = S.sifar_litmus(S.SIFAR_LITMUS_READ_FIRST, placement, PAIRS, TRIALS)
+    print(r, flush=True)
+    print(f"read-first violation rate {r['violations'] / r['trials']:.2e} "
+          f"({r['violations']} of {r['trials']}, {r['violations_first_epochs']} in the first "
+          f"two epochs)", flush=True)
+    assert r["timeouts"] == 0
+    assert r["trials"] == PAIRS * TRIALS
     if r["violations"]:
         g, found, want, _ = r["first_bad"]
         # a violation is a word of an earlier epoch of the same slot (or, in
