@@ -28,6 +28,8 @@ FLAGS = [
     "-ffp-contract=off",
     # no packed fp32 instructions (v_pk_add_f32 and friends) in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # leading scalar kernel arguments preloaded into SGPRs at wave start
+    "-mllvm", "-amdgpu-kernarg-preload-count=16",
     "-Wall",
     "-Wno-unused-command-line-argument",
 ]

@@ -126,8 +126,10 @@ ProduceArgs produce_args(const sifar_t h, int32_t tokens, EpochRef ep, const uin
     a.entry_stride = entry_stride;
     a.rank_stride = rank_stride;
     a.entries = entries;
+    a.entries_div = make_div(static_cast<uint32_t>(entries));
     a.inject = h->inject;
     a.inject_entries = h->inject_entries;
+    a.inject_div = make_div(static_cast<uint32_t>(h->inject_entries > 0 ? h->inject_entries : 1));
     a.stage = h->inject ? h->stage : nullptr;
     a.err = h->state->err;
     return a;
@@ -143,11 +145,13 @@ ReduceArgs reduce_args(const sifar_t h, int32_t tokens, EpochRef ep) {
     a.log = h->log;
     a.stamp_log = h->stamp_log;
     a.log_epochs = h->cfg.log_epochs;
+    a.log_div = make_div(static_cast<uint32_t>(h->cfg.log_epochs));
     a.max_attempts = h->cfg.max_attempts;
     a.forced_retries = h->cfg.forced_retries;
     a.spin_limit = h->cfg.spin_limit;
     a.inject = h->inject;
     a.inject_entries = h->inject_entries;
+    a.inject_div = make_div(static_cast<uint32_t>(h->inject_entries > 0 ? h->inject_entries : 1));
     a.stage = h->inject ? h->stage : nullptr;
     a.exch = h->exch;
     a.groups_per_token = h->groups_per_token;

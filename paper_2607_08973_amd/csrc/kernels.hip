@@ -98,12 +98,15 @@ __device__ __forceinline__ uint32_t log_word(uint32_t attempts, uint32_t first, 
            ((last & 0xFFu) << 24);
 }
 
-// Ranks the injection table makes late (not withheld) at epoch g.
-__device__ __forceinline__ uint32_t late_ranks(const uint16_t *inject, int32_t entries, uint32_t g) {
-    if (!inject) return 0;
-    const uint32_t inj = inject[(g - 1u) % static_cast<uint32_t>(entries)];
-    return inj & ~(inj >> 8) & 0xFFu;
+// The injection table's word for epoch g (late | withheld << 8), 0 without a
+// table.
+__device__ __forceinline__ uint32_t inject_word(const uint16_t *inject, const DivU32 &div,
+                                                uint32_t g) {
+    return inject ? inject[mod_u32(g - 1u, div)] : 0u;
 }
+
+// Ranks an injection word makes late (not withheld).
+__device__ __forceinline__ uint32_t late_ranks(uint32_t inj) { return inj & ~(inj >> 8) & 0xFFu; }
 
 // ---------------------------------------------------------------------------
 // Producer side: the emulated peers.
@@ -124,7 +127,7 @@ __device__ __forceinline__ uint32_t lane_offset(const Geometry &geo, const Chunk
 template <int N>
 __device__ __forceinline__ void load_sources(const ProduceArgs &a, const Chunk &k, uint32_t g,
                                              V16 (&v)[N]) {
-    const uint32_t e = (g - 1u) % static_cast<uint32_t>(a.entries);
+    const uint32_t e = mod_u32(g - 1u, a.entries_div);
     const uint16_t *src = a.src + e * a.entry_stride + static_cast<int64_t>(chunk_first(a.geo, k));
     const uint32_t off = lane_offset(a.geo, k);
 #pragma unroll
@@ -153,7 +156,7 @@ template <int N>
 __device__ __forceinline__ void copy_chunk(const ProduceArgs &a, const Chunk &k, uint32_t g,
                                            uint32_t p, uint32_t staged = 0) {
     const Geometry &geo = a.geo;
-    const uint32_t e = (g - 1u) % static_cast<uint32_t>(a.entries);
+    const uint32_t e = mod_u32(g - 1u, a.entries_div);
     const uint16_t *src = a.src + e * a.entry_stride + static_cast<int64_t>(k.row);
     const uint64_t at = static_cast<uint64_t>(p) * geo.slot_elems + k.row;
     V16 v[N];
@@ -168,12 +171,8 @@ __device__ __forceinline__ void copy_chunk(const ProduceArgs &a, const Chunk &k,
     }
 }
 
-// Ranks whose stamp the injection table holds back at epoch g (late | withheld).
-__device__ __forceinline__ uint32_t held_back(const uint16_t *inject, int32_t entries, uint32_t g) {
-    if (!inject) return 0;
-    const uint32_t inj = inject[(g - 1u) % static_cast<uint32_t>(entries)];
-    return (inj | (inj >> 8)) & 0xFFu;
-}
+// Ranks whose stamp an injection word holds back (late | withheld).
+__device__ __forceinline__ uint32_t held_back(uint32_t inj) { return (inj | (inj >> 8)) & 0xFFu; }
 
 // Producer of one epoch in its own launch (eager calls, step graphs). With
 // deterministic injection a late rank's payload goes to the stage and its
@@ -190,30 +189,46 @@ __device__ __forceinline__ uint32_t held_back(const uint16_t *inject, int32_t en
 // chunk-fastest then token, the order the reduction numbers its chunks, so with
 // one wave per group the producer and the reduction of a chunk share an XCD.
 template <int N>
-__device__ __forceinline__ void produce_chunk(const ProduceArgs &a) {
+__device__ __forceinline__ void produce_chunk(const ProduceArgs &a, int G) {
     const int lane = threadIdx.x & (kLanes - 1);
     const Geometry &geo = a.geo;
-    const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x * (blockDim.x / kLanes) +
-                                                  threadIdx.x / kLanes, lane);
-    if (!k.active) return;
+    // The epoch first: the source address depends on it, and a uniform load
+    // ahead of anything that may write memory stays a scalar load.
     const uint32_t g = epoch_of(a.ep);
+    // Every other argument the wave reads before its source loads, requested
+    // in one batch: the compiler otherwise loads kernel arguments block by
+    // block, one memory round trip at a time (measured: 4-5 of them in a row
+    // before the sources were requested).
+    asm volatile("" ::"s"(geo.hidden), "s"(geo.segs), "s"(geo.w_max), "s"(geo.slot_elems),
+                 "s"(a.ep.base), "s"(a.ep.parity), "s"(a.slots), "s"(a.stamps),
+                 "s"(a.consumed), "s"(a.produced), "s"(a.src), "s"(a.entry_stride),
+                 "s"(a.rank_stride), "s"(a.entries_div.m), "s"(a.entries_div.sh1),
+                 "s"(a.entries_div.sh2), "s"(a.entries_div.d), "s"(a.inject), "s"(a.stage),
+                 "s"(a.ep.off));
+    const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x * G + threadIdx.x / kLanes, lane);
+    if (!k.active) return;
     const uint32_t p = a.ep.parity;
     const size_t pc = static_cast<size_t>(p) * geo.w_max + k.c;
     // Dual-buffer rule: the slot's previous epoch must have been consumed.
     const uint32_t prev = ld_relaxed(a.produced + pc);
     const uint32_t done = ld_relaxed(a.consumed + pc);
-    const uint32_t held = held_back(a.inject, a.inject_entries, g);
-    copy_chunk<N>(a, k, g, p, a.stage ? late_ranks(a.inject, a.inject_entries, g) : 0u);
+    const uint32_t inj = inject_word(a.inject, a.inject_div, g);
+    const uint32_t held = held_back(inj);
+    copy_chunk<N>(a, k, g, p, a.stage ? late_ranks(inj) : 0u);
     if (lane == 0 && prev != done) latch(a.err, kErrWaw, g, k.c, prev);
+    // The stamps follow the payload within the wave; the reduction reads them
+    // in a later launch, whose start makes them visible device-wide, so they
+    // need not be written past the L2 (an agent-scope store would make the
+    // launch wait for that before it can end).
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     uint32_t *stamp = a.stamps + pc * N;
-    if (lane < N && !((held >> lane) & 1u)) st_relaxed(stamp + lane, g);
-    if (lane == 0) st_relaxed(a.produced + pc, g);
+    if (lane < N && !((held >> lane) & 1u)) st_flag(stamp + lane, g, true);
+    if (lane == 0) st_flag(a.produced + pc, g, true);
 }
 
 template <int N>
 __global__ __launch_bounds__(1024) void produce_kernel(ProduceArgs a) {
-    produce_chunk<N>(a);
+    produce_chunk<N>(a, static_cast<int>(blockDim.x) / kLanes);
 }
 
 // ---------------------------------------------------------------------------
@@ -234,22 +249,38 @@ __device__ __forceinline__ void load_payload(V16 (&v)[N], const uint16_t *slot0,
 // then, after a release, their stamps are written. The retry must therefore
 // reload the payload to get the right sum. `st_first` / `st_last`: this
 // lane's stamp (lanes < N) at the first and at the last validation.
+// `base_v` is the launch's epoch base as loaded (g = base_v + the launch's
+// offset); its first use waits until the payload and stamp loads are issued.
 template <int N, int MODE, bool INJECT_HOOK>
-__device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint32_t g, uint32_t p,
-                                       int lane, V16 (&v)[N], uint32_t &attempts, uint32_t &first,
-                                       uint32_t &last, uint32_t &st_first, uint32_t &st_last) {
+__device__ __forceinline__ uint32_t gather(const ReduceArgs &a, const Chunk &k, uint32_t base_v,
+                                           uint32_t p, int lane, V16 (&v)[N], uint32_t &attempts,
+                                           uint32_t &first, uint32_t &last, uint32_t &st_first,
+                                           uint32_t &st_last) {
     const Geometry &geo = a.geo;
     const uint16_t *slot0 = a.slots + static_cast<uint64_t>(p) * geo.slot_elems + k.row;
     const uint64_t rank_step = 2 * geo.slot_elems;  // slots are [rank][parity]
     uint32_t *stamp = a.stamps + (static_cast<size_t>(p) * geo.w_max + k.c) * N;
+    // every lane loads a stamp (lanes >= N rank N - 1's, which the ballot
+    // ignores): no branch holds the loads back behind the epoch's arrival
+    const uint32_t *stamp_lane = stamp + (lane < N ? lane : N - 1);
 
     uint32_t st = 0;
     if (MODE == kOrdered) {
-        if (k.active && lane < N) st = ld_acquire(stamp + lane);
+        st = ld_acquire(stamp_lane);
     } else {
         load_payload<N>(v, slot0, rank_step);
-        if (MODE == kSpec && k.active && lane < N) st = ld_relaxed(stamp + lane);
+        if (MODE == kSpec) st = ld_relaxed(stamp_lane);
     }
+    // nothing that needs the epoch may move ahead of these loads (the compiler
+    // otherwise waits for the epoch's load before it issues them)
+    __builtin_amdgcn_sched_barrier(0);
+    // the arguments needed once the payload is in, requested in one batch
+    // while it travels (the compiler would otherwise load them one round trip
+    // at a time where each is first used)
+    asm volatile("" ::"s"(a.consumed), "s"(a.log), "s"(a.stamp_log), "s"(a.log_div.m),
+                 "s"(a.log_div.sh1), "s"(a.log_div.sh2), "s"(a.log_div.d),
+                 "s"(a.forced_retries), "s"(a.out), "s"(a.max_attempts), "s"(a.inject));
+    const uint32_t g = base_v + a.ep.off;
     st_first = st;
 
     attempts = 1;
@@ -264,7 +295,7 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
                 break;
             }
             if (INJECT_HOOK && attempts == 1 && a.inject && m != 0) {
-                const uint32_t late = late_ranks(a.inject, a.inject_entries, g);
+                const uint32_t late = late_ranks(inject_word(a.inject, a.inject_div, g));
                 if (a.stage) {
                     const uint64_t at = static_cast<uint64_t>(p) * geo.slot_elems + k.row;
 #pragma unroll
@@ -283,9 +314,9 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
             // peers' data
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             if (MODE == kOrdered) {
-                if (lane < N) st = ld_acquire(stamp + lane);
+                st = ld_acquire(stamp_lane);
             } else {
-                if (lane < N) st = ld_relaxed(stamp + lane);
+                st = ld_relaxed(stamp_lane);
                 load_payload<N>(v, slot0, rank_step);
             }
             ++attempts;
@@ -296,6 +327,7 @@ __device__ __forceinline__ void gather(const ReduceArgs &a, const Chunk &k, uint
     }
     st_last = st;
     if (MODE == kOrdered) load_payload<N>(v, slot0, rank_step);
+    return g;
 }
 
 // Persistent-step gather of an active chunk: a producer may be writing right
@@ -368,7 +400,7 @@ __device__ __forceinline__ V16 sum_round(const V16 (&v)[N]) {
 
 __device__ __forceinline__ void write_log(const ReduceArgs &a, const Chunk &k, uint32_t g,
                                           uint32_t word) {
-    a.log[static_cast<size_t>((g - 1u) % static_cast<uint32_t>(a.log_epochs)) * a.geo.w_max + k.c] =
+    a.log[static_cast<size_t>(mod_u32(g - 1u, a.log_div)) * a.geo.w_max + k.c] =
         word;
 }
 
@@ -378,7 +410,7 @@ template <int N>
 __device__ __forceinline__ void write_stamp_log(const ReduceArgs &a, const Chunk &k, uint32_t g,
                                                 int r, uint32_t first, uint32_t last) {
     uint32_t *row = a.stamp_log +
-                    (static_cast<size_t>((g - 1u) % static_cast<uint32_t>(a.log_epochs)) *
+                    (static_cast<size_t>(mod_u32(g - 1u, a.log_div)) *
                          a.geo.w_max + k.c) * (2 * N) + r;
     row[0] = first;
     row[N] = last;
@@ -470,16 +502,51 @@ __device__ __forceinline__ void residual_rmsnorm(const ReduceArgs &a, const Chun
 // that write the NEXT epoch (other parity) while the first plane reduces this
 // one -- the emulated peers running one epoch ahead, which is as far ahead as
 // two slots allow. The planes touch disjoint slots and stamps.
+//
+// The arguments both planes need first come as the kernel's leading scalar
+// arguments: gfx950 can preload leading kernel arguments into scalar
+// registers when a wave starts (the build asks the compiler for it), so the
+// epoch's location and the slot and stamp addresses are known without a
+// memory round trip. `shape` packs hidden (bits 0-16), chunks per token (bits
+// 17-24), the consumer's slot parity (bit 25) and log2 of the waves per
+// workgroup (bits 26-28). The structs carry the rest, read later.
 template <int N, int MODE, bool EPI, bool FUSED>
-__global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs pa) {
+__global__ __launch_bounds__(1024) void reduce_kernel(const uint32_t *ep_base, uint16_t *slots,
+                                                      uint32_t *stamps, uint64_t slot_elems,
+                                                      uint32_t shape, uint32_t w_max,
+                                                      uint32_t ep_off, ReduceArgs ra,
+                                                      ProduceArgs pa) {
+    const int hidden = static_cast<int>(shape & 0x1FFFFu);
+    const int segs = static_cast<int>((shape >> 17) & 0xFFu);
+    const int G = 1 << ((shape >> 26) & 7u);
     if (FUSED && blockIdx.z == 1) {
-        produce_chunk<N>(pa);
+        ProduceArgs pp = pa;
+        pp.geo.hidden = hidden;
+        pp.geo.segs = segs;
+        pp.geo.w_max = static_cast<int32_t>(w_max);
+        pp.geo.slot_elems = slot_elems;
+        pp.ep.base = ep_base;
+        pp.slots = slots;
+        pp.stamps = stamps;
+        produce_chunk<N>(pp, G);
         return;
     }
+    ReduceArgs a = ra;
+    a.geo.hidden = hidden;
+    a.geo.segs = segs;
+    a.geo.w_max = static_cast<int32_t>(w_max);
+    a.geo.slot_elems = slot_elems;
+    a.ep.base = ep_base;
+    a.ep.off = ep_off;
+    a.ep.parity = (shape >> 25) & 1u;
+    a.slots = slots;
+    a.stamps = stamps;
     const int lane = threadIdx.x & (kLanes - 1);
     const int wave = threadIdx.x / kLanes;
-    const int G = blockDim.x / kLanes;
     const Geometry &geo = a.geo;
+    // The epoch base is read first: its address is at hand, and a uniform
+    // load ahead of anything that may write memory stays a scalar load.
+    const uint32_t base_v = ep_base[0];
     // grid: x = chunk groups of a token, y = token
     const Chunk k = chunk_at(geo, blockIdx.y, blockIdx.x * G + wave, lane);
     if (!EPI && !k.active) return;  // EPI: idle waves still join the barriers
@@ -490,10 +557,10 @@ __global__ __launch_bounds__(1024) void reduce_kernel(ReduceArgs a, ProduceArgs 
         rv = ld16(a.residual + k.row);
         wv = ld16(a.weight + k.elem);
     }
-    const uint32_t g = epoch_of(a.ep);
     V16 v[N];
     uint32_t attempts, first, last, st_first, st_last;
-    gather<N, MODE, true>(a, k, g, p, lane, v, attempts, first, last, st_first, st_last);
+    const uint32_t g =
+        gather<N, MODE, true>(a, k, base_v, p, lane, v, attempts, first, last, st_first, st_last);
     const V16 o = sum_round<N>(v);
     if (k.active && lane == 0) {
         write_log(a, k, g, log_word(attempts, first, last));
@@ -669,7 +736,8 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
             if (lane == 0) latch(a.err, kErrWaw, g, k.c, spins);
             return false;
         }
-        const uint32_t held = held_back(a.inject, a.inject_entries, g);
+        const uint32_t inj = inject_word(a.inject, a.inject_div, g);
+        const uint32_t held = held_back(inj);
         if (!PREFETCH) {
             copy_chunk<N>(a, k, g, p);
             publish_slot(local);
@@ -692,7 +760,6 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
         if (lane < N && !((held >> lane) & 1u)) st_flag(stamp + lane, g, local);
         if (lane == 0) st_flag(a.produced + pc, g, local);
         if (held) {
-            const uint32_t inj = a.inject[(g - 1u) % static_cast<uint32_t>(a.inject_entries)];
             for (uint32_t d = 0; d < A.late_delay; ++d) __builtin_amdgcn_s_sleep(8);
             if (lane < N && ((inj >> lane) & 1u) && !((inj >> (8 + lane)) & 1u))
                 st_flag(stamp + lane, g, local);
@@ -761,13 +828,13 @@ __device__ __forceinline__ void chain_producer_grouped(const ChainArgs &A, uint3
         __builtin_amdgcn_s_waitcnt(0);  // this wave's slot stores have reached L2
         if (__syncthreads_or(!free)) return;
         if (wave == 0) {
-            const uint32_t held = held_back(a.inject, a.inject_entries, g);
+            const uint32_t inj = inject_word(a.inject, a.inject_div, g);
+            const uint32_t held = held_back(inj);
             publish_slot(local);  // with `local` the wait above already did it
             const size_t ps = static_cast<size_t>(p) * geo.w_max + ks.c;
             uint32_t *stamp = a.stamps + ps * N;
             if (stamper && !((held >> sr) & 1u)) st_flag(stamp + sr, g, local);
             if (held) {
-                const uint32_t inj = a.inject[(g - 1u) % static_cast<uint32_t>(a.inject_entries)];
                 for (uint32_t d = 0; d < A.late_delay; ++d) __builtin_amdgcn_s_sleep(8);
                 if (stamper && ((inj >> sr) & 1u) && !((inj >> (8 + sr)) & 1u))
                     st_flag(stamp + sr, g, local);
@@ -953,18 +1020,38 @@ template <int N, int MODE>
 hipError_t launch_reduce_nm(const ReduceArgs &a, const ProduceArgs *pa, bool epi, dim3 grid,
                             dim3 block, hipStream_t s) {
     const ProduceArgs none{};
+    int lg = 0;
+    while ((kLanes << lg) < static_cast<int>(block.x)) ++lg;
+    if ((kLanes << lg) != static_cast<int>(block.x) || lg > 4) return hipErrorInvalidValue;
+    if (a.geo.hidden < 1 || a.geo.hidden > 0x10000 || a.geo.segs < 1 || a.geo.segs > 0xFF ||
+        a.ep.parity > 1)
+        return hipErrorInvalidValue;
+    // the producer plane shares the leading arguments (one handle's slots,
+    // stamps, epoch and geometry)
+    if (pa && (pa->ep.base != a.ep.base || pa->slots != a.slots || pa->stamps != a.stamps ||
+               pa->geo.hidden != a.geo.hidden || pa->geo.w_max != a.geo.w_max ||
+               pa->geo.slot_elems != a.geo.slot_elems))
+        return hipErrorInvalidValue;
+    const uint32_t shape = static_cast<uint32_t>(a.geo.hidden) |
+                           (static_cast<uint32_t>(a.geo.segs) << 17) | (a.ep.parity << 25) |
+                           (static_cast<uint32_t>(lg) << 26);
+    const uint32_t w_max = static_cast<uint32_t>(a.geo.w_max);
+#define SIFAR_REDUCE_LAUNCH(EPI_, FUSED_, PA_)                                                   \
+    hipLaunchKernelGGL((reduce_kernel<N, MODE, EPI_, FUSED_>), grid, block, 0, s, a.ep.base,   \
+                       a.slots, a.stamps, a.geo.slot_elems, shape, w_max, a.ep.off, a, PA_)
     if (pa) {
         grid.z = 2;
         if (epi)
-            hipLaunchKernelGGL((reduce_kernel<N, MODE, true, true>), grid, block, 0, s, a, *pa);
+            SIFAR_REDUCE_LAUNCH(true, true, *pa);
         else
-            hipLaunchKernelGGL((reduce_kernel<N, MODE, false, true>), grid, block, 0, s, a, *pa);
+            SIFAR_REDUCE_LAUNCH(false, true, *pa);
     } else {
         if (epi)
-            hipLaunchKernelGGL((reduce_kernel<N, MODE, true, false>), grid, block, 0, s, a, none);
+            SIFAR_REDUCE_LAUNCH(true, false, none);
         else
-            hipLaunchKernelGGL((reduce_kernel<N, MODE, false, false>), grid, block, 0, s, a, none);
+            SIFAR_REDUCE_LAUNCH(false, false, none);
     }
+#undef SIFAR_REDUCE_LAUNCH
     return hipGetLastError();
 }
 

@@ -104,6 +104,8 @@ extern "C" int sifar_allreduce_noalloc(const void *src, int64_t src_rank_stride,
     pa.entry_stride = 0;
     pa.rank_stride = src_rank_stride;
     pa.entries = 1;
+    pa.entries_div = make_div(1);
+    pa.inject_div = make_div(1);
     pa.err = state->err;
 
     ReduceArgs ra{};
@@ -114,6 +116,8 @@ extern "C" int sifar_allreduce_noalloc(const void *src, int64_t src_rank_stride,
     ra.consumed = reinterpret_cast<uint32_t *>(base + kOffConsumed);
     ra.log = reinterpret_cast<uint32_t *>(base + kOffLog);
     ra.log_epochs = 1;
+    ra.log_div = make_div(1);
+    ra.inject_div = make_div(1);
     ra.max_attempts = kAttempts;
     ra.spin_limit = 1;
     ra.out = static_cast<uint16_t *>(out);

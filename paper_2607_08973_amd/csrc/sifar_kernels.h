@@ -15,6 +15,32 @@ constexpr int kMaxWavesPerGroup = 16;
 constexpr int kChainGroupWaves = 4;         // waves per persistent-step workgroup when grouped
 constexpr int kExchPlanes = 4;              // epoch-indexed planes of the epilogue exchange
 
+// x % d for a divisor fixed per launch, by a multiply-high instead of a
+// division sequence (Granlund and Montgomery, "Division by invariant integers
+// using multiplication", 1994, unsigned case): with l = ceil(log2 d) and
+// m = floor(2^32 (2^l - d) / d) + 1, the quotient of a 32-bit x is
+// (t + ((x - t) >> min(l, 1))) >> max(l - 1, 0), t = the high word of m * x.
+struct DivU32 {
+    uint32_t m, sh1, sh2, d;
+};
+
+__host__ __device__ inline DivU32 make_div(uint32_t d) {
+    uint32_t l = 0;
+    while (l < 32 && (uint64_t{1} << l) < d) ++l;
+    DivU32 v;
+    v.m = static_cast<uint32_t>(((uint64_t{1} << 32) * ((uint64_t{1} << l) - d)) / d + 1);
+    v.sh1 = l < 1 ? l : 1;
+    v.sh2 = l > 1 ? l - 1 : 0;
+    v.d = d;
+    return v;
+}
+
+__host__ __device__ inline uint32_t mod_u32(uint32_t x, const DivU32 &v) {
+    const uint32_t t = static_cast<uint32_t>((static_cast<uint64_t>(v.m) * x) >> 32);
+    const uint32_t q = (t + ((x - t) >> v.sh1)) >> v.sh2;
+    return x - q * v.d;
+}
+
 // Device-resident state shared by all kernels of a handle.
 struct DevState {
     uint32_t epoch_base;   // graph nodes compute g = epoch_base + node offset
@@ -53,8 +79,10 @@ struct ProduceArgs {
     int64_t entry_stride;
     int64_t rank_stride;
     int32_t entries;             // epoch g uses entry (g - 1) % entries
+    DivU32 entries_div;          // make_div(entries)
     const uint16_t *inject;      // [inject_entries] late | withheld << 8, or null
     int32_t inject_entries;
+    DivU32 inject_div;           // make_div(inject_entries), or make_div(1) without a table
     uint16_t *stage;             // [N][2][slot_elems], or null: with deterministic injection a
                                  // late rank's payload is written here, not into its slot, and
                                  // the reduction moves it into the slot when the rank catches up
@@ -71,11 +99,13 @@ struct ReduceArgs {
     uint32_t *stamp_log;         // [log_epochs][w_max][2][N]: the raw stamps of the chunk's first
                                  // and last validation (per-epoch launches: may be null)
     int32_t log_epochs;
+    DivU32 log_div;              // make_div(log_epochs)
     uint32_t max_attempts;
     uint32_t forced_retries;
     uint32_t spin_limit;
     const uint16_t *inject;
     int32_t inject_entries;
+    DivU32 inject_div;
     const uint16_t *stage;       // late ranks' payload (ProduceArgs::stage), or null
     uint16_t *out;               // plain: [tokens][hidden]
     uint16_t *residual;          // epilogue: [tokens][hidden], in place
