@@ -82,6 +82,15 @@ __device__ __forceinline__ void st16(uint16_t *p, const V16 &v) {
     *reinterpret_cast<V16 *>(p) = v;
 }
 
+// A 16-byte store of data no wave of the launch reads again (an all-reduce
+// output): non-temporal, so that a large output stream does not push the slots
+// and sources that every epoch re-reads out of the caches.
+__device__ __forceinline__ void st16_stream(uint16_t *p, const V16 &v) {
+    const V4i x = {static_cast<int>(v.w[0]), static_cast<int>(v.w[1]), static_cast<int>(v.w[2]),
+                   static_cast<int>(v.w[3])};
+    __builtin_nontemporal_store(x, reinterpret_cast<V4i *>(p));
+}
+
 __device__ __forceinline__ uint32_t ld_relaxed(const uint32_t *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }

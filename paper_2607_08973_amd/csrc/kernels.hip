@@ -568,7 +568,7 @@ __global__ __launch_bounds__(1024) void reduce_kernel(const uint32_t *ep_base, u
     }
     if (a.stamp_log && k.active && lane < N) write_stamp_log<N>(a, k, g, lane, st_first, st_last);
     if (!EPI) {
-        if (k.lane_ok) st16(a.out + k.row, o);
+        if (k.lane_ok) st16_stream(a.out + k.row, o);
         return;
     }
     residual_rmsnorm(a, k, g, o, rv, wv, a.y, lane, wave, G, blockIdx.x);
@@ -927,7 +927,7 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
             // Lanes past the end of the row loaded the row's last 8 elements
             // (clamped) with the same instruction as the lane that owns them,
             // so they store the same bytes to the same place: no branch.
-            st16(a.out + ring + k.row, o);
+            st16_stream(a.out + ring + k.row, o);
         } else {
             EpiPending cur;
             epi_stage(a, k, g, o, rv, lane, wave, G, bx, xlocal, cur);
