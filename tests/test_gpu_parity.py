@@ -839,3 +839,30 @@ def test_single_buffer_epilogue_persistent():
         assert ulp_distance(y_got[i, :T], y_list[i]).max() <= 1
     run.s.check()
     run.s.close()
+
+
+def test_two_persistent_handles_step_concurrently():
+    """Two handles whose persistent steps are enqueued on two streams at once
+    (default priority), small enough that both steps' waves are resident
+    together: each handle's chain is its own (own slots, stamps and epoch
+    counter), so both sequences of outputs equal the oracle's."""
+    wa = synth.Workload(80, "concurrent-a", 8, (1,), 4096, 64, 1, "act")
+    wb = synth.Workload(81, "concurrent-b", 4, (2,), 2048, 32, 1, "normal")
+    ra = StepRun(wa, 1, persistent=1)
+    rb = StepRun(wb, 2, persistent=1)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for step in range(10):
+        with torch.cuda.stream(sa):
+            ea = ra.step(1)
+        with torch.cuda.stream(sb):
+            eb = rb.step(2)
+    torch.cuda.synchronize()
+    print("two handles: 10 concurrent steps each", flush=True)
+    for run, epochs, T in ((ra, ea, 1), (rb, eb, 2)):
+        run.s.check()
+        got = to_host(run.out_d)
+        exp = oracle.reduce_chain(run.pool, epochs, T)
+        for i in range(run.L):
+            assert np.array_equal(got[i, :T], exp[i]), (run.w.name, i)
+        run.s.close()
