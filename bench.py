@@ -866,7 +866,9 @@ def main():
         "floors": floors,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 3), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 6),
-                     "traffic": traffic, "bytes_per_launch": round(mean_bytes),
+                     "traffic": traffic, "traffic_scope": "hardware byte counters of the whole "
+                                                          "launch, the peers' copies included",
+                     "bytes_per_launch": round(mean_bytes),
                      "bytes": "one consumer's share per all-reduce: read N*K, write K, "
                               "4*N bytes of stamps per 512-element chunk; times the "
                               "all-reduces per launch",

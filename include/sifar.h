@@ -25,7 +25,7 @@
  *
  * The N ranks are emulated on one GPU: each rank's slots are HBM buffers, and
  * a producer kernel plays the peers, copying each rank's partial into its slot
- * and then release-storing its stamp. One process, one GPU; nothing crosses a
+ * and then storing its stamp after it. One process, one GPU; nothing crosses a
  * device boundary.
  *
  * Conventions
@@ -178,9 +178,10 @@ void sifar_destroy(sifar_t h);
 /* The emulated peers write epoch g = next produced epoch. Rank r's partial is
  * read from src + r * src_rank_stride (elements), laid out [tokens][hidden]
  * bf16, and copied into rank r's slot of parity g & 1; then rank r's stamps of
- * every chunk are set to g with release semantics (Sec. 4.1: "after the
- * preceding operation writes its result ... each GPU writes a flag"), except
- * for ranks the injection table marks late or withheld.
+ * every chunk are set to g, ordered after the payload within the producing
+ * wave and published device-wide by the end of the launch (Sec. 4.1: a rank
+ * raises its flag only once its partial is in the payload buffer), except for
+ * ranks the injection table marks late or withheld.
  * 1 <= tokens <= max_tokens; src_rank_stride >= tokens * hidden, multiple of 8. */
 int sifar_produce(sifar_t h, const void *src, int64_t src_rank_stride, int32_t tokens,
                   void *stream);
