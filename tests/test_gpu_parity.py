@@ -866,3 +866,33 @@ def test_two_persistent_handles_step_concurrently():
         for i in range(run.L):
             assert np.array_equal(got[i, :T], exp[i]), (run.w.name, i)
         run.s.close()
+
+
+@pytest.mark.parametrize("G", [2, 8, 16])
+@pytest.mark.parametrize("mode", ["spec", "ordered"])
+def test_graph_steps_multiwave_groups(G, mode):
+    """Per-launch steps with several waves per workgroup: the shape word the
+    kernel receives as a preloaded argument carries log2 of the waves per
+    group, and rows of 9 and 3 chunks leave idle waves in the last group of
+    each token (they must load in bounds and store nothing). Every output of
+    two steps per batch size."""
+    w = synth.Workload(82, f"multiwave-g{G}", 8, (1, 5), 4608, 8, 1, "act")
+    run = StepRun(w, 5, validate=mode, waves_per_group=G, pool=synth.payload_pool(82, 8, 5, 4608, 7, "act"))
+    for T in (1, 5):
+        for rep in range(2):
+            epochs = run.step(T)
+            got = to_host(run.out_d)
+            exp = oracle.reduce_chain(run.pool, epochs, T)
+            for i in range(w.reduces_per_step):
+                assert np.array_equal(got[i, :T], exp[i]), (G, mode, T, rep, i)
+    run.s.check()
+    run.s.close()
+    w2 = synth.Workload(83, f"multiwave-small-g{G}", 3, (2,), 1032, 6, 1, "normal")
+    run2 = StepRun(w2, 2, validate=mode, waves_per_group=G, pool=synth.payload_pool(83, 3, 2, 1032, 5, "normal"))
+    epochs = run2.step(2)
+    got = to_host(run2.out_d)
+    exp = oracle.reduce_chain(run2.pool, epochs, 2)
+    for i in range(w2.reduces_per_step):
+        assert np.array_equal(got[i, :2], exp[i]), (G, mode, "small", i)
+    run2.s.check()
+    run2.s.close()
