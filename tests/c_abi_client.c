@@ -11,8 +11,10 @@
  * The program reduces entry e as epoch e + 1 with eager sifar_produce /
  * sifar_reduce calls, then binds the E entries as a step's source pool and
  * runs one decode step of L all-reduces (PERSISTENT 1: one persistent launch,
- * ORDERED validation; 0: a captured per-epoch graph, SPEC validation). out.bin
- * receives the E eager outputs and then the L step outputs, T x H each.
+ * ORDERED validation; 0: a captured per-epoch graph, SPEC validation), then
+ * reduces every entry once more with sifar_allreduce_noalloc (no handle, no
+ * allocation). out.bin receives the E eager outputs, the L step outputs and
+ * the E allocation-free outputs, T x H each.
  * Returns 0 on success, 2 on a bad argument or file, 1 when a HIP or libsifar
  * call fails (after printing which).
  */
@@ -65,7 +67,7 @@ int sifar_c_client(int argc, char **argv) {
         return 2;
     }
     const size_t e_count = (size_t)bytes / (entry * 2);
-    const size_t outs = e_count + (size_t)l;
+    const size_t outs = 2 * e_count + (size_t)l;
     host_in = malloc((size_t)bytes);
     host_out = malloc(outs * row * 2);
     const int read_ok = host_in && host_out && fread(host_in, 1, (size_t)bytes, f) == (size_t)bytes;
@@ -110,6 +112,16 @@ int sifar_c_client(int argc, char **argv) {
     CHECK_HIP(hipMemcpy(host_out, out, outs * row * 2, hipMemcpyDeviceToHost));
     uint32_t next_prod = 0, next_red = 0;
     CHECK_SIFAR(sifar_epochs(h, &next_prod, &next_red));
+
+    /* the allocation-free entry point: every entry once more, queued back to
+       back on the null stream, after the step's outputs were copied out */
+    uint16_t *na = out + (e_count + (size_t)l) * row;
+    for (size_t e = 0; e < e_count; ++e)
+        CHECK_SIFAR(sifar_allreduce_noalloc(src + e * entry, (int64_t)row, n, t, hd, na + e * row,
+                                            NULL));
+    CHECK_HIP(hipDeviceSynchronize());
+    CHECK_HIP(hipMemcpy(host_out + (e_count + (size_t)l) * row, na, e_count * row * 2,
+                        hipMemcpyDeviceToHost));
 
     f = fopen(argv[7], "wb");
     if (!f) {

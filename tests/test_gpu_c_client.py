@@ -1,6 +1,7 @@
 """GPU: a C11 client of the C ABI (tests/c_abi_client.c) -- no Python or
-PyTorch between it and libsifar -- reduces seeded partials eagerly and in one
-decode step; its outputs are checked bit for bit against the oracle."""
+PyTorch between it and libsifar -- reduces seeded partials eagerly, in one
+decode step and through the allocation-free entry point; its outputs are
+checked bit for bit against the oracle."""
 from __future__ import annotations
 
 import ctypes
@@ -47,13 +48,15 @@ def test_c_client_matches_oracle(client, tmp_path, N, T, H, L, persistent):
     rc = run_client(client, ["c_abi_client", str(N), str(T), str(H), str(L), str(persistent),
                              str(src), str(dst)])
     assert rc == 0
-    got = np.fromfile(dst, dtype=np.uint16).reshape(E + L, T, H)
+    got = np.fromfile(dst, dtype=np.uint16).reshape(2 * E + L, T, H)
     for e in range(E):                       # eager epochs 1..E
         assert np.array_equal(got[e], oracle.reduce(pool[e])), f"eager epoch {e + 1}"
     base = E + (E & 1)                       # a step starts at an even epoch base
     for i in range(L):
         g = base + i + 1
         assert np.array_equal(got[E + i], oracle.reduce(pool[(g - 1) % E])), f"step node {i}"
+    for e in range(E):                       # sifar_allreduce_noalloc, entry by entry
+        assert np.array_equal(got[E + L + e], oracle.reduce(pool[e])), f"allocation-free {e}"
 
 
 def test_c_client_reports_bad_arguments(client, tmp_path):
