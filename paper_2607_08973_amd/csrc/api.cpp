@@ -172,18 +172,18 @@ int launch_red(sifar_t h, const ReduceArgs &ra, const ProduceArgs *next, hipStre
 }
 
 // Waves per workgroup of a persistent step. Grouping lets one publication
-// (and, for a cross-XCD pair, one release fence) cover 4 chunks and shares a
-// CU among 4 waves. Measured on MI355X with same-XCD pairs and the producer
-// loading each epoch's sources ahead (payload sweep, us per all-reduce,
-// one-wave vs grouped): plain steps at 512 chunks 1.81 vs 1.98 (N = 8), at
-// 1024 chunks 1.84 vs 1.98 (N = 2) but 4.32 vs 3.66 (N = 8), at 2048 chunks
-// 4.50 vs 3.84 (N = 2) and 10.5 vs 9.3 (N = 8); with the epilogue (MoE,
-// 512 chunks) 3.06 vs 2.80. So plain steps group from 1024 chunks at
-// N >= 8 and from 2048 below; epilogue steps from 512.
+// (and, for a cross-XCD pair, one release fence) cover 4 chunks, and the
+// epilogue's groups share one exchange word. Measured on MI355X (payload
+// sweep shapes, us per all-reduce, one-wave vs grouped): plain steps at 1024
+// chunks 2.88 vs 2.87 (N = 8) and 1.25 vs 1.59 (N = 4), at 2048 chunks
+// 1.58 vs 1.85 (N = 2), 3.05 vs 2.95 (N = 4) and 8.2 vs 7.9 (N = 8), at
+// 4096 chunks 3.41 vs 3.64 (N = 2), 7.53 vs 7.99 (N = 4) and 15.3 vs 16.4
+// (N = 8); with the epilogue (MoE, 512 chunks) 3.06 vs 2.80. So plain steps
+// run one wave per workgroup, epilogue steps group from 512 chunks.
 int chain_waves(const sifar_ctx *h, int32_t tokens) {
     const int64_t chunks = static_cast<int64_t>(tokens) * h->segs;
-    const int64_t from = h->cfg.epilogue ? 512 : (h->cfg.nranks >= 8 ? 1024 : 2048);
-    return h->chain_grouping && h->segs % kChainGroupWaves == 0 && chunks >= from
+    return h->cfg.epilogue && h->chain_grouping && h->segs % kChainGroupWaves == 0 &&
+                   chunks >= 512
                ? kChainGroupWaves
                : 1;
 }
@@ -363,8 +363,9 @@ int sifar_init(const sifar_config *cfg, sifar_t *out) {
             delete h;
             return SIFAR_EINVAL;
         }
-        const int gcap = max_active_chain_groups(c.nranks, c.validate, c.epilogue != 0,
-                                                 kChainGroupWaves, false);
+        const int gcap = c.epilogue ? max_active_chain_groups(c.nranks, c.validate, true,
+                                                              kChainGroupWaves, false)
+                                    : 0;
         h->chain_grouping = c.nranks * kChainGroupWaves <= kLanes && gcap > 0 &&
                             waves / kChainGroupWaves <= gcap;
     }

@@ -67,6 +67,18 @@ __device__ void latch(uint32_t *err, uint32_t kind, uint32_t g, uint32_t c, uint
 
 constexpr uint32_t kErrRetryBudget = 1, kErrWaw = 2, kErrExchange = 3;
 
+// A persistent step's waits read the error word only once they have lasted
+// this many polls, and no wave reads it otherwise: a healthy epoch needs one
+// or two polls, so the word is never read, while a wave whose wait outlasts
+// the step's failure elsewhere still leaves within microseconds. The word is
+// one address for the whole GPU: read by every consumer wave once per epoch
+// (beside its first stamp poll) it bounded the step as the chunks grew.
+// Measured on MI355X (llama8b decode, N = 8, H = 4096, us per all-reduce):
+// reading it with every poll, 0.794 at T = 1..8 / 1.01 at 16 tokens / 2.15 at
+// 64 tokens; only after 64 polls, 0.784 / 0.98 / 2.13 while consumers still
+// read it once per epoch; not per epoch either, 0.760 / 0.80 / 1.12.
+constexpr uint32_t kErrPollAfter = 64;
+
 // Where the calling lane works: token t, chunk s of the row, chunk index c.
 // Lanes past the end of the row load a clamped, in-bounds address (the row's
 // last 8 elements) and do not store (lane_ok false) -- except where a store of
@@ -337,9 +349,11 @@ __device__ __forceinline__ uint32_t gather(const ReduceArgs &a, const Chunk &k, 
 // N - 1's, which the ballot ignores) until every stamp is fresh, then the
 // payload is loaded -- after an acquire fence when the producer is on another
 // XCD, directly when it shares this XCD (see publish_slot). On return `st`
-// holds the stamp of the last poll.
+// holds the stamp of the last poll; the result is true when the wait failed:
+// the retry budget ran out (latched here), or an error latched elsewhere was
+// found while waiting.
 template <int N>
-__device__ __forceinline__ void gather_chain(const ReduceArgs &a, const Chunk &k, uint32_t g,
+__device__ __forceinline__ bool gather_chain(const ReduceArgs &a, const Chunk &k, uint32_t g,
                                              uint32_t p, int lane, uint32_t m, uint32_t &st,
                                              V16 (&v)[N], uint32_t &attempts, uint32_t &first,
                                              uint32_t &last, bool local) {
@@ -355,24 +369,30 @@ __device__ __forceinline__ void gather_chain(const ReduceArgs &a, const Chunk &k
     attempts = 1;
     first = last = m;
     bool fail = m != 0 || a.forced_retries >= 1;
+    bool failed = false;
     while (fail) {
         if (attempts >= a.max_attempts) {
             if (lane == 0) latch(a.err, kErrRetryBudget, g, k.c, attempts);
+            failed = true;
             break;
         }
-        // one round trip per poll, the stamps and the error word together,
-        // back to back (a short sleep between polls measured ~2 % slower)
-        const uint32_t e = ld_relaxed(a.err);
+        // one round trip per poll, back to back (a short sleep between polls
+        // measured ~2 % slower); the error word joins it after kErrPollAfter
+        const uint32_t e = attempts >= kErrPollAfter ? ld_relaxed(a.err) : 0u;
         st = ld_relaxed(stamp);
         ++attempts;
         m = static_cast<uint32_t>(__ballot(lane < N && st != g));
         last = m;
-        if (m != 0 && e != 0) break;  // the step is already failing: stop waiting
+        if (m != 0 && e != 0) {  // the step is already failing: stop waiting
+            failed = true;
+            break;
+        }
         fail = m != 0 || attempts <= a.forced_retries;
     }
     acquire_slot(local);
 #pragma unroll
     for (int r = 0; r < N; ++r) v[r] = ld16_agent(chunk0 + r * rank_step, off);
+    return failed;
 }
 
 // Fixed-order fp32 sum: acc = x_0; acc += x_1; ... acc += x_{N-1}; then bf16.
@@ -635,12 +655,15 @@ __device__ __forceinline__ void epi_stage(const ReduceArgs &a, const Chunk &k, u
 }
 
 // `y` is the ring entry of epoch pd.g. (`pd` by value: with a reference the
-// compiler kept the pending state in scratch memory.)
-__device__ __forceinline__ void epi_finish(const ReduceArgs &a, const Chunk &k,
+// compiler kept the pending state in scratch memory.) True in wave 0 when the
+// exchange wait failed: it ran out of polls (latched here), or found an error
+// latched elsewhere.
+__device__ __forceinline__ bool epi_finish(const ReduceArgs &a, const Chunk &k,
                                            const EpiPending pd, const V16 &wv, uint16_t *y,
                                            int lane, int wave) {
     const int Q = a.groups_per_token;
     float tot = pd.grp;
+    bool failed = false;
     if (Q > 1) {
         __shared__ float total;
         if (wave == 0) {
@@ -654,7 +677,9 @@ __device__ __forceinline__ void epi_finish(const ReduceArgs &a, const Chunk &k,
                 if (lane < Q)
                     mine = __hip_atomic_load(ex + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 ready = __ballot(lane < Q && static_cast<uint32_t>(mine >> 32) != pd.g) == 0;
+                if (!ready && spins >= kErrPollAfter && ld_relaxed(a.err) != 0) break;
             } while (!ready && ++spins < a.spin_limit);
+            failed = !ready;
             if (!ready && lane == 0) latch(a.err, kErrExchange, pd.g, k.c, spins);
             const float pv = __uint_as_float(static_cast<uint32_t>(mine));
             float sum = 0.f;
@@ -672,6 +697,7 @@ __device__ __forceinline__ void epi_finish(const ReduceArgs &a, const Chunk &k,
         yo.w[i] = pack_bf16((pd.x[2 * i] * inv) * w0, (pd.x[2 * i + 1] * inv) * w1);
     }
     if (k.lane_ok) st16(y + k.row, yo);
+    return failed;
 }
 
 // ---------------------------------------------------------------------------
@@ -721,13 +747,14 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
         const size_t pc = static_cast<size_t>(p) * geo.w_max + k.c;
         uint32_t spins = 0;
         bool free = false;
-        // one round trip per poll: both words and the error word together; a
-        // short sleep between polls (without it the kernel takes 109 VGPRs
-        // instead of 76 and the step ran ~0.6 % slower)
+        // one round trip per poll: both words together, and the error word
+        // after kErrPollAfter polls; a short sleep between polls (without it
+        // the kernel takes 109 VGPRs instead of 76 and the step ran ~0.6 %
+        // slower)
         while (true) {
             const uint32_t done = ld_relaxed(a.consumed + pc);
             const uint32_t prev = ld_relaxed(a.produced + pc);
-            const uint32_t e = ld_relaxed(a.err);
+            const uint32_t e = spins >= kErrPollAfter ? ld_relaxed(a.err) : 0u;
             free = done == prev;
             if (free || ++spins >= A.r.spin_limit || e != 0) break;
             __builtin_amdgcn_s_sleep(1);
@@ -810,7 +837,7 @@ __device__ __forceinline__ void chain_producer_grouped(const ChainArgs &A, uint3
             while (true) {  // one round trip per poll, as in chain_producer
                 const uint32_t done = ld_relaxed(a.consumed + pc);
                 const uint32_t prev = ld_relaxed(a.produced + pc);
-                const uint32_t e = ld_relaxed(a.err);
+                const uint32_t e = spins >= kErrPollAfter ? ld_relaxed(a.err) : 0u;
                 free = done == prev;
                 if (free || ++spins >= A.r.spin_limit || e != 0) break;
                 __builtin_amdgcn_s_sleep(1);
@@ -869,15 +896,14 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
     // which the ballot ignores), so no branch surrounds the poll.
     const uint32_t *stamps = a.stamps + static_cast<size_t>(k.c) * N + (lane < N ? lane : N - 1);
     const size_t parity_stride = static_cast<size_t>(geo.w_max) * N;
-    // The first poll of an epoch -- its stamps and the error word -- is issued
-    // before the previous epoch's stores. On gfx9-family GPUs one counter
+    // The first poll of an epoch -- its stamps -- is issued before the
+    // previous epoch's stores. On gfx9-family GPUs one counter
     // (vmcnt) tracks loads and stores in issue order, so a poll issued after
     // the stores could only be waited for together with their write
     // acknowledgements. The stores below are therefore branch-free too, so the
     // compiler can count them and wait for the poll alone. An early poll that
     // reads stale is repeated; the payload is still loaded only after fresh
     // stamps were seen.
-    uint32_t err_word = ld_relaxed(a.err);
     uint32_t st_next = ld_relaxed(stamps + (1u & A.parity_mask) * parity_stride);
     // stale ranks of the first poll, evaluated where the wait for it is exact
     uint32_t m_next = static_cast<uint32_t>(__ballot(lane < N && st_next != base + 1u));
@@ -890,20 +916,16 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
         uint32_t attempts, first, last;
         const uint32_t st_first = st_next;
         uint32_t st_last = st_next;
-        gather_chain<N>(a, k, g, p, lane, m_next, st_last, v, attempts, first, last, local);
+        bool stop =
+            gather_chain<N>(a, k, g, p, lane, m_next, st_last, v, attempts, first, last, local);
         uint32_t *consumed = a.consumed + static_cast<size_t>(p) * geo.w_max + k.c;
-        bool stop = false;
-        // Once the payload has arrived: note the error word read with this
-        // epoch's first poll (loads return in order, so it has arrived too),
-        // issue the next epoch's first polls (harmless in-bounds reads after
-        // the last epoch), then release the slot (every lane stores the same
-        // word).
+        // Once the payload has arrived: issue the next epoch's first poll (a
+        // harmless in-bounds read after the last epoch), then release the slot
+        // (every lane stores the same word).
         auto poll_next_and_release = [&]() {
-            stop = err_word != 0;
             const uint32_t pn = static_cast<uint32_t>(i + 2) & A.parity_mask;
-            err_word = ld_relaxed(a.err);
             st_next = ld_relaxed(stamps + pn * parity_stride);
-            __atomic_signal_fence(__ATOMIC_SEQ_CST);  // keep the polls ahead of the stores
+            __atomic_signal_fence(__ATOMIC_SEQ_CST);  // keep the poll ahead of the stores
             st_flag(consumed, g, local);
         };
         if (!EPI) {
@@ -931,15 +953,19 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
         } else {
             EpiPending cur;
             epi_stage(a, k, g, o, rv, lane, wave, G, bx, xlocal, cur);
-            if (have_pending) epi_finish(a, k, pending, wv, a.y + ring - A.ring_stride, lane, wave);
+            if (have_pending &&
+                epi_finish(a, k, pending, wv, a.y + ring - A.ring_stride, lane, wave))
+                stop = true;
             pending = cur;
             have_pending = true;
         }
         // The next epoch's first poll, after this epoch's stores: the
         // compiler waits for the poll alone and leaves the stores in flight.
         m_next = static_cast<uint32_t>(__ballot(lane < N && st_next != g + 1u));
-        // a bounded wait failed somewhere: stop the step (a pending epilogue
-        // stays unwritten: the step has failed)
+        // a bounded wait of this wave failed: stop (a pending epilogue stays
+        // unwritten: the step has failed). Every wait is bounded and reads the
+        // error word once it has lasted kErrPollAfter polls, so a failure
+        // anywhere ends the other waves' waits too.
         if (GROUPED && EPI) {
             if (__syncthreads_or(stop)) return;
         } else if (stop) {
@@ -951,19 +977,16 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
                    lane, wave);
 }
 
-// Grid (segs / G, tokens, 2) of G-wave workgroups (G = 1, or kChainGroupWaves
-// when GROUPED), or (8 * ceil(tokens / 8) * Q, 1, 2) with the epilogue (Q =
-// segs / G, layout below): plane 0 reduces chunk (t, x * G + wave) for epochs
-// base+1 .. base+L in order, plane 1 produces it. The last wave to arrive on
-// the counter advances the epoch base for the next step: every wave read the
-// base before it arrived, so no wave can see the advanced value.
-// The plain grouped form is held to 64 VGPRs (8 waves per SIMD; 3 registers
-// spill, outside the epoch loop) so that the payload sweep's 4096-chunk step
-// (2048 four-wave groups) fits the GPU grouped: 22.4 -> 21.0 us per
-// all-reduce against the one-wave form it needed at 68 VGPRs.
+// Grid (segs, tokens, 2) of one-wave workgroups, or with the epilogue
+// (8 * ceil(tokens / 8) * Q, 1, 2) of G-wave workgroups (G = 1, or
+// kChainGroupWaves when GROUPED; Q = segs / G, layout below): plane 0 reduces
+// chunk (t, x * G + wave) for epochs base+1 .. base+L in order, plane 1
+// produces it. The last wave to arrive on the counter advances the epoch base
+// for the next step: every wave read the base before it arrived, so no wave
+// can see the advanced value.
 template <int N, int MODE, bool EPI, bool GROUPED, bool PREFETCH>
 __global__ __launch_bounds__(GROUPED ? kChainGroupWaves * kLanes : kLanes,
-                             GROUPED && !EPI ? 8 : 1) void chain_kernel(ChainArgs A) {
+                             1) void chain_kernel(ChainArgs A) {
     const int lane = threadIdx.x & (kLanes - 1);
     const int wave = GROUPED ? static_cast<int>(threadIdx.x) / kLanes : 0;
     const int G = GROUPED ? static_cast<int>(blockDim.x) / kLanes : 1;
@@ -1066,14 +1089,15 @@ hipError_t launch_reduce_n(const ReduceArgs &a, const ProduceArgs *pa, int mode,
     return hipErrorInvalidValue;
 }
 
-// The grouped producer loads and stores in one go; with the epilogue the
-// consumer sets the register count, so only the plain one-wave-per-chunk
-// kernel comes in both producer forms.
+// Grouped workgroups serve epilogue steps only (plain steps measured faster
+// or level with one wave per workgroup); the grouped producer loads and
+// stores in one go. With the epilogue the consumer sets the register count,
+// so only the plain one-wave-per-chunk kernel comes in both producer forms.
 template <int N, int MODE>
 const void *chain_fn(bool epi, bool grouped, bool prefetch) {
     if (grouped)
         return epi ? reinterpret_cast<const void *>(chain_kernel<N, MODE, true, true, false>)
-                   : reinterpret_cast<const void *>(chain_kernel<N, MODE, false, true, false>);
+                   : nullptr;
     if (epi) return reinterpret_cast<const void *>(chain_kernel<N, MODE, true, false, true>);
     return prefetch ? reinterpret_cast<const void *>(chain_kernel<N, MODE, false, false, true>)
                     : reinterpret_cast<const void *>(chain_kernel<N, MODE, false, false, false>);

@@ -480,6 +480,31 @@ def test_epilogue_widest_rows(N, T, H, persistent, G):
     run.s.close()
 
 
+@pytest.mark.parametrize("N,T,H", [(5, 64, 3896), (3, 130, 2040)])
+def test_persistent_epilogue_grouped_ragged(N, T, H):
+    """Persistent residual-add + RMSNorm steps from 512 chunks run in 4-wave
+    workgroups: 3896 leaves a partial last chunk inside each token's last
+    group; 130 tokens pad the grid to 136 (one XCD per token), so the padding
+    tokens' workgroups only arrive on the counter. Two steps of 8 chained
+    nodes: residual bit-exact, y within 1 bf16 step."""
+    w = synth.Workload(97 + N, f"epilogue-grouped-n{N}-t{T}-h{H}", N, (T,), H, 8, 2, "act",
+                       epilogue=True)
+    run = StepRun(w, T, persistent=1, pool=synth.payload_pool(w.wid, N, T, H, 5, w.dist))
+    res = run.res0[:T].copy()
+    for step in range(2):
+        print(f"epilogue grouped N={N} T={T} H={H} step {step}", flush=True)
+        epochs = run.step(T)
+        y_got = to_host(run.y_d)
+        _, r_list, y_list = oracle.reduce_chain(run.pool, epochs, T,
+                                                epilogue=(res, run.weight, w.rms_eps))
+        assert np.array_equal(to_host(run.res_d)[:T], r_list[-1])
+        for i in range(w.reduces_per_step):
+            assert ulp_distance(y_got[i, :T], y_list[i]).max() <= 1, f"step {step} node {i}"
+        res = r_list[-1]
+    run.s.check()
+    run.s.close()
+
+
 @pytest.mark.parametrize("H,persistent,G", [(65536, 0, 1), (32776, 1, 1), (65536, 1, 4)])
 def test_epilogue_rows_beyond_the_exchange_are_refused(H, persistent, G):
     """More than 64 groups per token (or, persistent, more than 64 chunks) would
@@ -574,8 +599,7 @@ def test_steps_with_a_changing_batch_size(persistent):
 def test_persistent_late_stamps(T):
     """Late ranks' stamps land after a delay while the reduction waits on them:
     outputs equal the oracle; the decision log shows retries and ends clean.
-    T = 8 (64 chunks) runs the grouped producer: one release fence and one
-    stamping wave per 4-chunk workgroup."""
+    (The grouped producer meets late stamps in the epilogue tests below.)"""
     w = synth.SPEC_STRESS
     steps = 6
     late = synth.delay_table(w.wid, w.nranks, w.reduces_per_step * steps, w.stale_prob)
@@ -597,16 +621,18 @@ def test_persistent_late_stamps(T):
     assert retried > 0
 
 
-@pytest.mark.parametrize("T,H", [(2, 1024), (8, 4096)])
-def test_persistent_withheld_stamp_latches(T, H):
+@pytest.mark.parametrize("T,H,epilogue", [(2, 1024, False), (8, 4096, False), (64, 4096, True)])
+def test_persistent_withheld_stamp_latches(T, H, epilogue):
     """A stamp that never lands ends the step with a latched error instead of
-    a hang; (8, 4096) is 64 chunks, the grouped producer."""
-    w = synth.Workload(70, "withheld", 4, (T,), H, 8, 1, "normal")
+    a hang. With the epilogue, 64 tokens x 8 chunks run in 4-wave workgroups:
+    the grouped producer, and groups that wait for each other's sums of
+    squares while their own wait fails."""
+    w = synth.Workload(70, "withheld", 4, (T,), H, 8, 1, "normal", epilogue=epilogue)
     run = StepRun(w, T, persistent=1, max_attempts=64, spin_limit=1 << 14)
     table = [0] * 16
     table[4] = 0b0010 << 8      # epoch 5: rank 1's stamp never lands
     run.s.set_injection(table)
-    print(f"withheld T={T} H={H}", flush=True)
+    print(f"withheld T={T} H={H} epilogue={epilogue}", flush=True)
     run.step(T)
     assert run.s.status() == S.SIFAR_EDEVICE
     kind, epoch, chunk, attempts = run.s.error_info()
@@ -704,13 +730,12 @@ def test_persistent_late_stamps_log_replay(T):
                                    (1, 4, 2048), (7, 2, 4096), (6, 128, 4096)])
 def test_persistent_ragged_shapes(N, T, H):
     """Persistent steps on shapes off the benchmark grid: 3896 leaves a partial
-    last chunk inside a grouped workgroup (8 chunks per token, 128 chunks);
-    4608 has 9 chunks per token, not divisible into 4-wave workgroups, so the
-    step falls back to one wave per workgroup; N = 3 with 64 chunks groups too.
-    The next four have a number of workgroups per plane that is not a multiple
-    of the 8 XCDs (2, 9, 1 and 45 chunks), so a chunk's producer and consumer
-    run on different XCDs and meet only through agent-scope memory. Then one
-    rank, an odd rank count, and 1024 chunks in 4-wave workgroups at N = 6."""
+    last chunk in each row (8 chunks per token, 128 chunks); 4608 has 9 chunks
+    per token; N = 3 with 64 chunks. The next four have a number of workgroups
+    per plane that is not a multiple of the 8 XCDs (2, 9, 1 and 45 chunks), so
+    a chunk's producer and consumer run on different XCDs and meet only through
+    agent-scope memory. Then one rank, an odd rank count, and 1024 chunks at
+    N = 6."""
     w = synth.Workload(73, f"ragged-{N}-{T}-{H}", N, (T,), H, 12, 1, "normal")
     run = StepRun(w, T, persistent=1)
     for rep in range(3):
