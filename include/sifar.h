@@ -244,7 +244,9 @@ int sifar_bind_step(sifar_t h, const sifar_step_buffers *b);
  * A persistent step needs all its waves resident at once (checked at init
  * against an otherwise idle GPU); persistent steps of several handles that run
  * concurrently on different streams may not fit together, and then end with a
- * latched SIFAR_EDEVICE (every wait is bounded) instead of completing. */
+ * latched SIFAR_EDEVICE (every wait is bounded) instead of completing. Once one
+ * wave of a persistent step has latched an error, the others end within
+ * microseconds: a wait that has lasted 64 polls also reads the error word. */
 int sifar_step(sifar_t h, int32_t tokens, void *stream);
 
 /* ---- injection, logs, state --------------------------------------------------- */
