@@ -711,10 +711,12 @@ __device__ __forceinline__ bool epi_finish(const ReduceArgs &a, const Chunk &k,
 //             only when the consumer is on another XCD), store the on-time
 //             stamps and produced[p] = g; injected late ranks' stamps follow
 //             after `late_delay` sleeps.
-//   consumer  poll the stamps (relaxed agent-scope loads, backoff) until all
-//             are fresh, then load the payload (after an acquire fence when
-//             the producer is on another XCD); sum; store; consumed[p] = g
-//             once every payload load has completed.
+//   consumer  poll the stamps (relaxed agent-scope loads, back to back) until
+//             all are fresh, then load the payload (after an acquire fence
+//             when the producer is on another XCD); sum; store; consumed[p] =
+//             g once every payload load has completed.
+// Every wait is bounded, and joins the error word to its polls only once it
+// has lasted kErrPollAfter polls.
 // Validation comes before the payload loads here (ORDERED). Speculative
 // payload loads issued alongside the stamp loads were measured to return a
 // rank's previous epoch while its stamp already read as fresh when producer
@@ -806,7 +808,8 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
     }
 }
 
-// Grouped producer (G waves per workgroup, one chunk per wave): the waves
+// Grouped producer of epilogue steps (G waves per workgroup, one chunk per
+// wave): the waves
 // copy their chunks, wait until their stores have reached L2, meet at a
 // workgroup barrier, and wave 0 publishes for all of them (one agent-scope
 // release fence, needed only when a consumer of the group is on another XCD)
