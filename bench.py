@@ -658,8 +658,9 @@ def suite(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: this build runs on a single MI355X and has no "
-              f"multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
+        print(f"bench.py measures one GPU: the library emulates the N ranks on a single "
+              f"MI355X and has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
         sys.exit(2)
     if args.workload != "llama8b-decode":
         import torch
