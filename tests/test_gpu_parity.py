@@ -921,3 +921,52 @@ def test_graph_steps_multiwave_groups(G, mode):
         assert np.array_equal(got[i, :2], exp[i]), (G, mode, "small", i)
     run2.s.check()
     run2.s.close()
+
+
+def _random_shapes(n=12, seed=2607):
+    """Seeded shapes off every grid: N = 1..8 ranks, rows of 8..9000 elements
+    (ragged last chunks), 1..48 tokens (at most 1024 chunks), with or without
+    the epilogue, 3..8 all-reduces per step."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < n:
+        N = int(rng.integers(1, 9))
+        H = 8 * int(rng.integers(1, 1126))
+        T = int(rng.integers(1, 49))
+        if T * -(-H // 512) > 1024:
+            continue
+        cases.append((N, T, H, bool(rng.integers(0, 2)), int(rng.integers(3, 9))))
+    return cases
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_random_shapes_both_step_forms(case):
+    """The same seeded shape as a captured per-launch step (SPEC) and as a
+    persistent step (ORDERED), two steps each: every all-reduce output
+    bit-exact, or with the epilogue the residual bit-exact and every y within
+    1 bf16 step."""
+    N, T, H, epi, L = _random_shapes()[case]
+    for persistent in (0, 1):
+        w = synth.Workload(120 + case, f"random-{case}", N, (T,), H, L, 2, "act", epilogue=epi)
+        run = StepRun(w, T, persistent=persistent,
+                      pool=synth.payload_pool(w.wid, N, T, H, 5, w.dist))
+        res = run.res0[:T].copy() if epi else None
+        for step in range(2):
+            print(f"random case {case}: N={N} T={T} H={H} epilogue={epi} L={L} "
+                  f"persistent={persistent} step {step}", flush=True)
+            epochs = run.step(T)
+            if epi:
+                y_got = to_host(run.y_d)
+                _, r_list, y_list = oracle.reduce_chain(run.pool, epochs, T,
+                                                        epilogue=(res, run.weight, w.rms_eps))
+                assert np.array_equal(to_host(run.res_d)[:T], r_list[-1]), (case, persistent, step)
+                for i in range(L):
+                    assert ulp_distance(y_got[i, :T], y_list[i]).max() <= 1, (case, persistent, step, i)
+                res = r_list[-1]
+            else:
+                got = to_host(run.out_d)
+                exp = oracle.reduce_chain(run.pool, epochs, T)
+                for i in range(L):
+                    assert np.array_equal(got[i, :T], exp[i]), (case, persistent, step, i)
+        run.s.check()
+        run.s.close()
