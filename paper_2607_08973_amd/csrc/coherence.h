@@ -71,6 +71,30 @@ __device__ __forceinline__ V16 ld16_agent(const void *base, uint32_t off) {
     return ld16_buffer<kCachePolicyAgent>(base, off);
 }
 
+// 16 bytes at byte offset off + soff through the descriptor rs, made once
+// for several loads (per load only the scalar offset soff changes), with
+// ld16_agent's caching: past this CU's L1.
+__device__ __forceinline__ V16 ld16_agent_at(__amdgpu_buffer_rsrc_t rs, uint32_t off,
+                                             uint32_t soff) {
+    const V4i x = __builtin_amdgcn_raw_buffer_load_b128(rs, static_cast<int>(off),
+                                                        static_cast<int>(soff), kCachePolicyAgent);
+    V16 v;
+    v.w[0] = static_cast<uint32_t>(x[0]);
+    v.w[1] = static_cast<uint32_t>(x[1]);
+    v.w[2] = static_cast<uint32_t>(x[2]);
+    v.w[3] = static_cast<uint32_t>(x[3]);
+    return v;
+}
+
+// 16 bytes to byte offset off + soff through the descriptor rs (normal
+// caching), made once for several stores.
+__device__ __forceinline__ void st16_at(__amdgpu_buffer_rsrc_t rs, uint32_t off, uint32_t soff,
+                                        const V16 &v) {
+    const V4i x = {static_cast<int>(v.w[0]), static_cast<int>(v.w[1]), static_cast<int>(v.w[2]),
+                   static_cast<int>(v.w[3])};
+    __builtin_amdgcn_raw_buffer_store_b128(x, rs, static_cast<int>(off), static_cast<int>(soff), 0);
+}
+
 // The store counterpart of ld16_buffer (normal caching).
 __device__ __forceinline__ void st16_buffer(void *base, uint32_t off, const V16 &v) {
     const V4i x = {static_cast<int>(v.w[0]), static_cast<int>(v.w[1]), static_cast<int>(v.w[2]),

@@ -146,6 +146,24 @@ __device__ __forceinline__ void load_sources(const ProduceArgs &a, const Chunk &
     for (int r = 0; r < N; ++r) v[r] = ld16_buffer<0>(src + r * a.rank_stride, off);
 }
 
+// The same through one descriptor, every rank's slot at a scalar offset from
+// rank 0's (launch_chain checks that the offsets fit): one scalar instruction
+// per store instead of three for a descriptor of its own, so the stores the
+// publication waits for leave back to back.
+template <int N>
+__device__ __forceinline__ void store_slots_at(const ProduceArgs &a, const Chunk &k, uint32_t p,
+                                               const V16 (&v)[N]) {
+    const Geometry &geo = a.geo;
+    const __amdgpu_buffer_rsrc_t rs =
+        buffer_rsrc(a.slots + static_cast<uint64_t>(p) * geo.slot_elems + chunk_first(geo, k));
+    const uint32_t off = lane_offset(geo, k);
+    const uint32_t rank_bytes = static_cast<uint32_t>(geo.slot_elems) * 4u;
+    if (k.lane_ok) {
+#pragma unroll
+        for (int r = 0; r < N; ++r) st16_at(rs, off, static_cast<uint32_t>(r) * rank_bytes, v[r]);
+    }
+}
+
 // ... written into the slots of parity p.
 template <int N>
 __device__ __forceinline__ void store_slots(const ProduceArgs &a, const Chunk &k, uint32_t p,
@@ -351,8 +369,15 @@ __device__ __forceinline__ uint32_t gather(const ReduceArgs &a, const Chunk &k, 
 // XCD, directly when it shares this XCD (see publish_slot). On return `st`
 // holds the stamp of the last poll; the result is true when the wait failed:
 // the retry budget ran out (latched here), or an error latched elsewhere was
-// found while waiting.
-template <int N>
+// found while waiting. With AT the payload loads share one descriptor, every
+// rank at a scalar offset, and leave back to back (a lone wave pays an issue
+// slot for every instruction: three scalar ones per descriptor kept the last
+// load ~50 ns behind the first). Epilogue kernels keep a descriptor per load:
+// their scalar registers are full, and the hoisted offsets spilled into 12
+// more vector registers. Measured with the producer's stores done the same
+// way (llama8b decode, us per all-reduce): 0.759 -> 0.721 at T = 1..8,
+// 0.80 -> 0.75 at 16 tokens, 1.13 -> 1.08 at 64 tokens.
+template <int N, bool AT>
 __device__ __forceinline__ bool gather_chain(const ReduceArgs &a, const Chunk &k, uint32_t g,
                                              uint32_t p, int lane, uint32_t m, uint32_t &st,
                                              V16 (&v)[N], uint32_t &attempts, uint32_t &first,
@@ -390,8 +415,16 @@ __device__ __forceinline__ bool gather_chain(const ReduceArgs &a, const Chunk &k
         fail = m != 0 || attempts <= a.forced_retries;
     }
     acquire_slot(local);
+    if (AT) {
+        const __amdgpu_buffer_rsrc_t rs = buffer_rsrc(chunk0);
+        const uint32_t rank_bytes = static_cast<uint32_t>(rank_step) * 2u;
 #pragma unroll
-    for (int r = 0; r < N; ++r) v[r] = ld16_agent(chunk0 + r * rank_step, off);
+        for (int r = 0; r < N; ++r)
+            v[r] = ld16_agent_at(rs, off, static_cast<uint32_t>(r) * rank_bytes);
+    } else {
+#pragma unroll
+        for (int r = 0; r < N; ++r) v[r] = ld16_agent(chunk0 + r * rank_step, off);
+    }
     return failed;
 }
 
@@ -771,7 +804,7 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
             copy_chunk<N>(a, k, g, p);
             publish_slot(local);
         } else if (local) {
-            store_slots<N>(a, k, p, cur);
+            store_slots_at<N>(a, k, p, cur);
             // the loads stay after the stores (the wait below counts on it)
             __atomic_signal_fence(__ATOMIC_SEQ_CST);
             load_sources<N>(a, k, g + 1u, nxt);
@@ -781,7 +814,7 @@ __device__ __forceinline__ void chain_producer(const ChainArgs &A, uint32_t base
             __builtin_amdgcn_s_waitcnt(kWaitVm | N);
             __atomic_signal_fence(__ATOMIC_SEQ_CST);
         } else {
-            store_slots<N>(a, k, p, cur);
+            store_slots_at<N>(a, k, p, cur);
             load_sources<N>(a, k, g + 1u, nxt);
             publish_slot(false);
         }
@@ -920,7 +953,7 @@ __device__ __forceinline__ void chain_consumer(const ChainArgs &A, uint32_t base
         const uint32_t st_first = st_next;
         uint32_t st_last = st_next;
         bool stop =
-            gather_chain<N>(a, k, g, p, lane, m_next, st_last, v, attempts, first, last, local);
+            gather_chain<N, !EPI>(a, k, g, p, lane, m_next, st_last, v, attempts, first, last, local);
         uint32_t *consumed = a.consumed + static_cast<size_t>(p) * geo.w_max + k.c;
         // Once the payload has arrived: issue the next epoch's first poll (a
         // harmless in-bounds read after the last epoch), then release the slot
@@ -1219,6 +1252,11 @@ hipError_t launch_chain(const ChainArgs &a, int mode, bool epilogue, int waves, 
     const uint32_t q = static_cast<uint32_t>(a.r.geo.segs / waves);
     const uint32_t t8 = (static_cast<uint32_t>(a.r.geo.tokens) + 7u) / 8u;
     if (epilogue && a.r.groups_per_token != static_cast<int32_t>(q)) return hipErrorInvalidValue;
+    // the slots are addressed at 32-bit offsets from rank 0's (payload loads,
+    // slot stores); co-residency keeps a step far below that (at most 4096
+    // chunks: under 64 MiB of slots)
+    if (static_cast<uint64_t>(a.r.geo.nranks) * 4u * a.r.geo.slot_elems > 0x7fffffffull)
+        return hipErrorInvalidValue;
     const dim3 grid = epilogue ? dim3(8u * t8 * q, 1, 2)
                                : dim3(q, static_cast<uint32_t>(a.r.geo.tokens), 2);
     void *args[] = {const_cast<ChainArgs *>(&a)};
